@@ -1,0 +1,164 @@
+"""fp64 oracle for the MoE expert FFN step (route → permute → grouped FFN →
+finalize).
+
+TEST INFRASTRUCTURE ONLY (see ``oracle/__init__.py``).
+
+Paper §IV-A optimises the decode-path kernels of the gpt-oss-20b MoE model on
+B200, among them "MoE finalize" (Table I): the routing-weighted sum of each
+token's top-k expert outputs, returned to token order. §V names the joint
+optimisation of the whole MoE-MLP block as the next step. The expert MLP of
+that model is a clamped SwiGLU: the gate is clamped above at ``limit``, the up
+projection to [−limit, limit], glu = gate·σ(α·gate) and the output is
+(up + 1)·glu, with α = 1.702 and limit = 7.
+
+The oracle takes the block's steps in order, each as its plain definition:
+
+  route     top-k of the E router logits per token, ordered by value
+            descending with ties to the lower expert index; routing weights
+            are the softmax over the k selected logits
+  permute   slot p = t·k + j carries expert idx[t, j]; counts[e] is the
+            histogram, offsets the exclusive prefix sum (length E + 1) and
+            perm lists the slot ids sorted by (expert, slot id) — a stable
+            sort, which makes it unique
+  expert e  X = x[perm[r] // k] for the rows r of expert e;
+            G = X·W_gu[e]ᵀ, gate | up = the two halves of G (or its even /
+            odd columns when interleaved); h = clamped SwiGLU(gate, up);
+            h is stored in the method's declared intermediate format
+            (bf16 RNE, or e4m3 with a per-row fp32 scale), modelled here;
+            y_slot[rows] = h·W_d[e]ᵀ
+  finalize  out[t] = Σ_j w[t, j]·y_slot[t·k + j], j ascending
+
+fp8 (W8A8) variant: weights are stored as e4m3 codes with one fp32 scale per
+output row (decoded before they reach this oracle); activations (x per
+token, h per slot row) are quantised online with s = amax/448 and
+code = RNE_sat(v / s). Those quantisation decisions are taken in fp32, the
+precision the kernel takes them in, so both sides pick the same code.
+"""
+
+import numpy as np
+
+from .codecs import (E4M3_MAX, bf16_decode, bf16_encode_rne, e4m3_decode,
+                     e4m3_encode_rne_sat, f32_round)
+
+
+def ref_route(logits, k):
+    """Top-k experts per token (descending, ties → lower index) and the
+    softmax over the selected logits (fp64)."""
+    logits = np.asarray(logits, dtype=np.float64)
+    T, E = logits.shape
+    idx = np.empty((T, k), dtype=np.int32)
+    for t in range(T):
+        order = sorted(range(E), key=lambda e: (-logits[t, e], e))
+        idx[t] = order[:k]
+    sel = np.take_along_axis(logits, idx.astype(np.int64), axis=1)
+    ex = np.exp(sel - sel.max(axis=1, keepdims=True))
+    w = ex / ex.sum(axis=1, keepdims=True)
+    return idx, w
+
+
+def ref_permute(idx, E):
+    """Expert histogram, exclusive offsets and the stable slot permutation."""
+    idx = np.asarray(idx)
+    T, k = idx.shape
+    flat = idx.reshape(-1)
+    counts = np.array([int(np.sum(flat == e)) for e in range(E)], dtype=np.int32)
+    offsets = np.zeros(E + 1, dtype=np.int32)
+    offsets[1:] = np.cumsum(counts)
+    perm = np.array(sorted(range(T * k), key=lambda p: (int(flat[p]), p)), dtype=np.int32)
+    return counts, offsets, perm
+
+
+def ref_swiglu_clamped(gate, up, alpha=1.702, limit=7.0):
+    """Clamped SwiGLU: (clip(up, −L, L) + 1) · g·σ(α·g), g = min(gate, L)."""
+    g = np.minimum(gate, limit)
+    u = np.clip(up, -limit, limit)
+    sig = 1.0 / (1.0 + np.exp(-alpha * g))
+    return (u + 1.0) * (g * sig)
+
+
+def ref_quant_rows_e4m3(v):
+    """Per-row e4m3 quantisation, decisions in fp32.
+
+    s = fp32(amax_row)/448 rounded to fp32 (a zero row gets s = 1);
+    code = RNE_sat_e4m3(fp32(fp32(v)/s)). Returns (codes uint8, s fp64)."""
+    v32 = f32_round(v)
+    amax = np.max(np.abs(v32), axis=-1, keepdims=True)
+    s = f32_round(amax / E4M3_MAX)
+    s = np.where(amax == 0.0, 1.0, s)
+    q = e4m3_encode_rne_sat(f32_round(v32 / s))
+    return q, s[..., 0]
+
+
+def _dequant_rows(codes, s):
+    return e4m3_decode(codes) * np.asarray(s, dtype=np.float64)[..., None]
+
+
+def _split_gate_up(G, I, interleaved):
+    if interleaved:
+        return G[:, 0::2], G[:, 1::2]
+    return G[:, :I], G[:, I:]
+
+
+def ref_expert_rows(X, W_gu, W_d, storage="bf16", act_quant=False, alpha=1.702,
+                    limit=7.0, interleaved=False):
+    """One expert's FFN over rows X [n, H] → y [n, H] (unweighted), fp64.
+
+    storage: "bf16" or "e4m3" — the declared format of the intermediate h.
+    act_quant: quantise X per row to e4m3 first (the W8A8 variant)."""
+    X = np.asarray(X, dtype=np.float64)
+    I = W_d.shape[1]
+    if act_quant:
+        q, s = ref_quant_rows_e4m3(X)
+        X = _dequant_rows(q, s)
+    G = X @ np.asarray(W_gu, dtype=np.float64).T
+    gate, up = _split_gate_up(G, I, interleaved)
+    h = ref_swiglu_clamped(gate, up, alpha, limit)
+    if storage == "bf16":
+        h = bf16_decode(bf16_encode_rne(h))
+    elif storage == "e4m3":
+        q, s = ref_quant_rows_e4m3(h)
+        h = _dequant_rows(q, s)
+    elif storage != "none":
+        raise ValueError(f"unknown storage {storage!r}")
+    return h @ np.asarray(W_d, dtype=np.float64).T
+
+
+def ref_moe(x, logits, weights, k, storage="bf16", act_quant=False, alpha=1.702,
+            limit=7.0, interleaved=False, tokens=None):
+    """The MoE expert FFN step, fp64.
+
+    x: [T, H] fp64 (decoded bf16 tokens); logits: [T, E] (fp32 values);
+    weights: callable e -> (W_gu [2I, H], W_d [H, I]) fp64 (decoded, scales
+    applied), or a pair of arrays [E, 2I, H], [E, H, I].
+    tokens: optional subset of token ids whose outputs to compute (a token's
+    output depends only on its own row and its own routing).
+    Returns a dict: out [T or len(tokens), H], idx, w, counts, offsets, perm.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    T, H = x.shape
+    E = np.asarray(logits).shape[1]
+    if not callable(weights):
+        Wgu_all, Wd_all = weights
+        weights = lambda e: (Wgu_all[e], Wd_all[e])  # noqa: E731
+    idx, w = ref_route(logits, k)
+    counts, offsets, perm = ref_permute(idx, E)
+    tok = np.arange(T) if tokens is None else np.asarray(tokens, dtype=np.int64)
+    # compact slot buffer: row c·k + j holds slot (tok[c], j)
+    row_of_token = np.full(T, -1, dtype=np.int64)
+    row_of_token[tok] = np.arange(tok.size)
+    y_slot = np.zeros((tok.size * k, H), dtype=np.float64)
+    for e in range(E):
+        slots = perm[offsets[e]:offsets[e + 1]].astype(np.int64)
+        slots = slots[row_of_token[slots // k] >= 0]
+        if slots.size == 0:
+            continue
+        W_gu, W_d = weights(e)
+        y = ref_expert_rows(x[slots // k], W_gu, W_d, storage, act_quant, alpha,
+                            limit, interleaved)
+        y_slot[row_of_token[slots // k] * k + slots % k] = y
+    # finalize: routing-weighted sum over the k slots of each token, j ascending
+    out = np.zeros((tok.size, H), dtype=np.float64)
+    for j in range(k):
+        out += w[tok, j][:, None] * y_slot[j::k]
+    return {"out": out, "idx": idx, "w": w, "counts": counts,
+            "offsets": offsets, "perm": perm}

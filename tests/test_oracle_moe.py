@@ -1,0 +1,271 @@
+"""Pins for the MoE oracle (``oracle.moe``).
+
+Routing is checked against its defining property (every unselected expert
+ranks below the last selected one under (value desc, index asc)) and closed
+forms (arange and all-equal logits); the permutation against its definition
+(a stable sort by expert); the clamped SwiGLU against its special values and
+mpmath; the whole block against a token-order brute force in mpmath that
+never builds the permutation, against the dense FFN it reduces to at E = 1,
+k = 1, and against the identical-experts and zero-W_down closed forms. The
+fp8 activation quantiser is pinned by the e4m3 grid and by its extreme code."""
+
+import math
+
+import mpmath as mp
+import numpy as np
+import pytest
+
+import oracle.moe as om
+from oracle.codecs import bf16_decode, bf16_encode_rne, e4m3_decode
+from oracle.fgemm import ref_fgemm
+from oracle.moe import (ref_moe, ref_permute, ref_quant_rows_e4m3, ref_route,
+                        ref_swiglu_clamped)
+from paper_2606_02963_amd.synth import MoeSpec, make_moe_activations, make_moe_weights
+
+mp.mp.dps = 50
+
+
+def _check_route_property(logits, idx, w):
+    T, E = logits.shape
+    k = idx.shape[1]
+    for t in range(T):
+        sel = list(idx[t])
+        assert len(set(sel)) == k
+        keys = [(logits[t, e], -e) for e in sel]
+        assert keys == sorted(keys, reverse=True)
+        last = keys[-1]
+        for e in range(E):
+            if e not in sel:
+                assert (logits[t, e], -e) < last
+    np.testing.assert_allclose(w.sum(1), 1.0, rtol=1e-15)
+    assert np.all(np.diff(w, axis=1) <= 0)
+
+
+def test_route_closed_forms():
+    lg = np.tile(np.arange(32, dtype=np.float64), (3, 1))
+    idx, w = ref_route(lg, 4)
+    assert idx.tolist() == [[31, 30, 29, 28]] * 3
+    e = np.exp([0.0, -1.0, -2.0, -3.0])
+    np.testing.assert_allclose(w, np.tile(e / e.sum(), (3, 1)), rtol=1e-15)
+    idx, w = ref_route(np.zeros((2, 32)), 4)
+    assert idx.tolist() == [[0, 1, 2, 3]] * 2
+    np.testing.assert_array_equal(w, 0.25)
+
+
+def test_route_defining_property_with_ties():
+    rng = np.random.default_rng(11)
+    lg = np.round(rng.standard_normal((200, 32)) * 2) / 2      # many exact ties
+    idx, w = ref_route(lg, 4)
+    _check_route_property(lg, idx, w)
+    lg = rng.standard_normal((300, 32)).astype(np.float32).astype(np.float64)
+    idx, w = ref_route(lg, 4)
+    _check_route_property(lg, idx, w)
+
+
+def test_route_weights_mpmath():
+    rng = np.random.default_rng(12)
+    lg = rng.standard_normal((5, 8))
+    idx, w = ref_route(lg, 3)
+    for t in range(5):
+        ex = [mp.exp(mp.mpf(float(lg[t, e]))) for e in idx[t]]
+        s = mp.fsum(ex)
+        np.testing.assert_allclose(w[t], [float(v / s) for v in ex], rtol=1e-15)
+
+
+def test_permute_definition():
+    rng = np.random.default_rng(13)
+    idx = rng.integers(0, 8, size=(50, 4)).astype(np.int32)
+    idx[:, 1] = (idx[:, 0] + 1) % 8        # keep experts distinct per token (not required)
+    counts, offsets, perm = ref_permute(idx, 10)   # experts 8, 9 empty
+    flat = idx.reshape(-1)
+    assert sorted(perm.tolist()) == list(range(200))
+    np.testing.assert_array_equal(counts, np.bincount(flat, minlength=10))
+    assert offsets[0] == 0 and offsets[-1] == 200
+    np.testing.assert_array_equal(np.diff(offsets), counts)
+    assert counts[8] == 0 and offsets[8] == offsets[9] == offsets[10]
+    for e in range(10):
+        seg = perm[offsets[e]:offsets[e + 1]]
+        assert np.all(flat[seg] == e)
+        assert np.all(np.diff(seg) > 0)       # stable: ascending slot id within an expert
+
+
+def test_swiglu_special_values_and_mpmath():
+    g = np.array([0.0, 1.0, 7.0, 8.0, 100.0, -3.0])
+    u = np.array([5.0, -1.0, 2.0, 2.0, 9.0, -9.0])
+    out = ref_swiglu_clamped(g, u)
+    assert out[0] == 0.0 and out[1] == 0.0                     # gate 0 / up −1 give 0
+    assert out[3] == out[2] and out[4] == ref_swiglu_clamped(np.array([7.0]), np.array([7.0]))[0]
+    assert out[5] == ref_swiglu_clamped(np.array([-3.0]), np.array([-7.0]))[0]
+    rng = np.random.default_rng(14)
+    gg, uu = rng.standard_normal(50) * 6, rng.standard_normal(50) * 6
+    got = ref_swiglu_clamped(gg, uu)
+    for i in range(50):
+        gm = min(mp.mpf(float(gg[i])), 7)
+        um = min(max(mp.mpf(float(uu[i])), -7), 7)
+        want = (um + 1) * gm / (1 + mp.exp(-mp.mpf("1.702") * gm))
+        assert abs(got[i] - float(want)) <= 1e-14 * max(1.0, abs(float(want)))
+
+
+def _mp_bruteforce_moe(x, lg, Wgu, Wd, k, alpha=1.702, limit=7.0):
+    """Token-order evaluation in mpmath: no histogram, no permutation."""
+    T, H = x.shape
+    E = lg.shape[1]
+    I = Wd.shape[2]
+    out = np.zeros((T, H))
+    for t in range(T):
+        order = sorted(range(E), key=lambda e: (-lg[t, e], e))[:k]
+        ex = [mp.exp(mp.mpf(float(lg[t, e]))) for e in order]
+        den = mp.fsum(ex)
+        acc = [mp.mpf(0)] * H
+        for j, e in enumerate(order):
+            xs = [mp.mpf(float(v)) for v in x[t]]
+            G = [mp.fsum(xs[c] * mp.mpf(float(Wgu[e, n, c])) for c in range(H)) for n in range(2 * I)]
+            h = []
+            for i in range(I):
+                gm = min(G[i], limit)
+                um = min(max(G[I + i], -limit), limit)
+                hv = (um + 1) * gm / (1 + mp.exp(-mp.mpf(alpha) * gm))
+                h.append(mp.mpf(float(bf16_decode(bf16_encode_rne(np.array([float(hv)])))[0])))
+            for n in range(H):
+                y = mp.fsum(h[i] * mp.mpf(float(Wd[e, n, i])) for i in range(I))
+                acc[n] += ex[j] / den * y
+        out[t] = [float(v) for v in acc]
+    return out
+
+
+def test_moe_bruteforce_token_order():
+    rng = np.random.default_rng(15)
+    T, H, I, E, k = 6, 4, 4, 4, 2
+    x = bf16_decode(bf16_encode_rne(rng.standard_normal((T, H)) * 2))
+    lg = rng.standard_normal((T, E)).astype(np.float32).astype(np.float64)
+    lg[2, :] = 0.5                                  # a fully tied row
+    Wgu = bf16_decode(bf16_encode_rne(rng.standard_normal((E, 2 * I, H))))
+    Wd = bf16_decode(bf16_encode_rne(rng.standard_normal((E, H, I))))
+    got = ref_moe(x, lg, (Wgu, Wd), k)["out"]
+    want = _mp_bruteforce_moe(x, lg, Wgu, Wd, k)
+    np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12)
+    # the token subset path returns the same rows
+    sub = ref_moe(x, lg, (Wgu, Wd), k, tokens=[4, 1])["out"]
+    np.testing.assert_allclose(sub, got[[4, 1]], rtol=0, atol=0)
+
+
+def test_moe_single_expert_is_dense_ffn():
+    rng = np.random.default_rng(16)
+    T, H, I = 9, 8, 6
+    x = rng.standard_normal((T, H))
+    Wgu = rng.standard_normal((1, 2 * I, H)) * 0.5
+    Wd = rng.standard_normal((1, H, I)) * 0.5
+    got = ref_moe(x, rng.standard_normal((T, 1)), (Wgu, Wd), 1, storage="none")["out"]
+    G = ref_fgemm(x, Wgu[0])
+    h = ref_swiglu_clamped(G[:, :I], G[:, I:])
+    np.testing.assert_allclose(got, ref_fgemm(h, Wd[0]), rtol=1e-14, atol=1e-14)
+
+
+def test_moe_identical_experts_and_zero_down():
+    rng = np.random.default_rng(17)
+    T, H, I, E = 7, 8, 4, 5
+    x = rng.standard_normal((T, H))
+    wgu1 = rng.standard_normal((2 * I, H))
+    wd1 = rng.standard_normal((H, I))
+    Wgu = np.stack([wgu1] * E)
+    Wd = np.stack([wd1] * E)
+    lg = rng.standard_normal((T, E))
+    got = ref_moe(x, lg, (Wgu, Wd), 3, storage="none")["out"]
+    G = x @ wgu1.T
+    want = ref_swiglu_clamped(G[:, :I], G[:, I:]) @ wd1.T
+    np.testing.assert_allclose(got, want, rtol=1e-13, atol=1e-13)
+    z = ref_moe(x, lg, (Wgu, np.zeros_like(Wd)), 3)["out"]
+    assert np.all(z == 0.0)
+
+
+def test_interleaved_gate_up_is_a_row_permutation():
+    rng = np.random.default_rng(18)
+    T, H, I = 5, 8, 4
+    x = rng.standard_normal((T, H))
+    Wgu = rng.standard_normal((1, 2 * I, H))
+    Wd = rng.standard_normal((1, H, I))
+    lg = np.zeros((T, 1))
+    a = ref_moe(x, lg, (Wgu, Wd), 1, storage="none")["out"]
+    inter = np.empty_like(Wgu)
+    inter[0, 0::2], inter[0, 1::2] = Wgu[0, :I], Wgu[0, I:]
+    b = ref_moe(x, lg, (inter, Wd), 1, storage="none", interleaved=True)["out"]
+    np.testing.assert_allclose(a, b, rtol=1e-15, atol=1e-15)
+
+
+def test_quant_rows_e4m3():
+    rng = np.random.default_rng(19)
+    v = rng.standard_normal((20, 300)) * rng.random((20, 1)) * 10
+    v[3] = 0.0
+    q, s = ref_quant_rows_e4m3(v)
+    d = e4m3_decode(q)
+    assert s[3] == 1.0 and np.all(q[3] == 0)
+    nz = np.arange(20) != 3
+    # the row maximum lands on the largest code, ±448
+    assert np.all(np.max(np.abs(d[nz]), 1) == 448.0)
+    # every value is within half an e4m3 step (relative 2^-4 for normals, 2^-10·s below)
+    err = np.abs(d * s[:, None] - v)
+    bound = np.maximum(np.abs(v) * 2.0 ** -4, s[:, None] * 2.0 ** -10) * (1 + 1e-6)
+    assert np.all(err <= bound)
+
+
+def test_planted_mistakes_are_caught(monkeypatch):
+    """Mistakes planted in the oracle on the CPU make a pin fail: unstable
+    permutation order, ties broken to the higher index, and a dropped +1 on
+    the up branch."""
+    orig_perm = om.ref_permute
+
+    def unstable_perm(idx, E):
+        counts, offsets, perm = orig_perm(idx, E)
+        out = perm.copy()
+        for e in range(E):
+            out[offsets[e]:offsets[e + 1]] = out[offsets[e]:offsets[e + 1]][::-1]
+        return counts, offsets, out
+    with pytest.raises(AssertionError):
+        test_permute_definition_via(unstable_perm)
+
+    def route_high_ties(logits, k):
+        logits = np.asarray(logits, dtype=np.float64)
+        T, E = logits.shape
+        idx = np.array([sorted(range(E), key=lambda e: (-logits[t, e], -e))[:k] for t in range(T)], dtype=np.int32)
+        sel = np.take_along_axis(logits, idx.astype(np.int64), 1)
+        ex = np.exp(sel - sel.max(1, keepdims=True))
+        return idx, ex / ex.sum(1, keepdims=True)
+    with pytest.raises(AssertionError):
+        lg = np.zeros((2, 32))
+        idx, _ = route_high_ties(lg, 4)
+        assert idx.tolist() == [[0, 1, 2, 3]] * 2
+
+    def swiglu_no_plus_one(gate, up, alpha=1.702, limit=7.0):
+        g = np.minimum(gate, limit)
+        return np.clip(up, -limit, limit) * g / (1 + np.exp(-alpha * g))
+    with monkeypatch.context() as m:
+        m.setattr(om, "ref_swiglu_clamped", swiglu_no_plus_one)
+        with pytest.raises(AssertionError):
+            test_moe_bruteforce_token_order()
+
+
+def test_permute_definition_via(fn=ref_permute):
+    rng = np.random.default_rng(20)
+    idx = rng.integers(0, 6, size=(40, 3)).astype(np.int32)
+    counts, offsets, perm = fn(idx, 6)
+    flat = idx.reshape(-1)
+    for e in range(6):
+        seg = perm[offsets[e]:offsets[e + 1]]
+        assert np.all(flat[seg] == e)
+        assert np.all(np.diff(seg) > 0)
+
+
+def test_synth_moe_shapes_small():
+    spec = MoeSpec("t", T=8, H=64, I=64, E=4, k=2)
+    a = make_moe_activations(spec, 0)
+    w = make_moe_weights(spec, 0)
+    assert a["x"].shape == (8, 64) and a["x"].dtype == np.uint16
+    assert w["w_gate_up"].shape == (4, 128, 64) and w["w_down"].shape == (4, 64, 64)
+    spec8 = MoeSpec("t8", T=8, H=64, I=64, E=4, k=2, w_dtype="e4m3")
+    w8 = make_moe_weights(spec8, 0)
+    assert w8["w_gate_up"].dtype == np.uint8 and w8["s_gate_up"].shape == (4, 128)
+    # the stored codes reproduce the fp32 draws to e4m3 precision
+    d = e4m3_decode(w8["w_gate_up"]) * w8["s_gate_up"][..., None]
+    wf = bf16_decode(w["w_gate_up"])
+    assert np.max(np.abs(d - wf)) <= 2.0 ** -4 * np.max(np.abs(wf)) + 1e-3
+    assert math.isfinite(float(d.sum()))
