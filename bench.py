@@ -1,0 +1,208 @@
+#!/usr/bin/env python3
+"""Benchmark: fused bf16 GEMM + GELU-tanh/clamp tail on one MI355X.
+
+Workload (the configuration the headline metric is quoted on):
+x[1024, 8192] ~ N(0,1), W[8192, 8192] and b[8192] ~ U(±1/√8192), bf16 inputs,
+y = clamp(GELU_tanh((x·Wᵀ + b)·0.5), −1, 1), bf16 output, fp32 accumulation.
+One step = one fused launch over that batch, inputs resident in HBM.
+
+Prints ONE JSON line with the fused kernel's TFLOP/s (``value``), its
+roofline fraction against the dense bf16 MFMA peak, the unfused sequence
+(vendor GEMM + one eager kernel per tail op) and the GEMM alone timed beside
+it, and the fp64 CPU oracle timed on a bounded sample of rows.
+
+Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
+"""
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published
+PEAK_HBM_GBS = 8000.0
+PROFILES = os.path.join(ROOT, "profiles")
+KERNEL_SOURCES = ["fg_tile.hpp", "fg_epilogue.hpp", "fgemm.hip"]
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-unfused", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample time")
+    return ap.parse_args()
+
+
+def kernel_source_hash():
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2606_02963_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(name):
+    """HBM bytes per launch from committed rocprofv3 --pmc summaries
+    (FETCH_SIZE + WRITE_SIZE, copy-kernel calibrated) if they were taken on
+    the current kernel sources; None otherwise."""
+    path = os.path.join(PROFILES, f"{name}.pmc.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as fh:
+        d = json.load(fh)
+    if d.get("kernel_source_hash") != kernel_source_hash():
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def time_steps(fn, steps, warmup, torch):
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(steps):
+        fn()
+    stop.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(stop) / steps      # ms per step
+
+
+def cpu_oracle_baseline(spec, inp, budget_s, gpu_out_rows):
+    """Time the fp64 oracle on a growing sample of rows until ~budget_s."""
+    import numpy as np
+    from threadpoolctl import threadpool_info
+    from oracle import bf16_decode, compare, ref_fgemm
+
+    x64 = bf16_decode(inp["x"])
+    W64 = bf16_decode(inp["W"])
+    b = inp["b"].astype(np.float64)
+    rows = 8
+    t_total, flops_total, n_rows = 0.0, 0.0, 0
+    first_ref = None
+    while t_total < budget_s and n_rows < spec.M:
+        r = min(rows, spec.M - n_rows)
+        sel = slice(n_rows, n_rows + r)
+        t0 = time.perf_counter()
+        ref = ref_fgemm(x64[sel], W64, b, spec.ops)
+        dt = time.perf_counter() - t0
+        if first_ref is None:
+            first_ref = ref
+        t_total += dt
+        flops_total += 2.0 * r * spec.N * spec.K
+        n_rows += r
+        rows *= 2
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    rep = compare(gpu_out_rows[: first_ref.shape[0]], first_ref, "bf16")
+    return {"value": flops_total / t_total / 1e12, "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"{n_rows} of {spec.M} output rows (all {spec.N} columns, K={spec.K}), fp64 numpy "
+                      f"matmul + tail, {t_total:.1f} s",
+            "seconds": round(t_total, 2)}, rep
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+                          "n_gpus": args.gpus}))
+        print("bench.py: multi-GPU runs are not part of this build (one GPU per box); use --gpus 1",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import torch.nn.functional as F
+
+    from paper_2606_02963_amd import _lib, api
+    from paper_2606_02963_amd.synth import FGEMM_SPECS, make_fgemm_inputs
+
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    _lib.lib()   # fail loudly if the HIP library is missing
+
+    spec = FGEMM_SPECS["bf16_gelu_clamp"]
+    inp = make_fgemm_inputs(spec, seed=0)
+    dev = torch.device("cuda", 0)
+    x = torch.from_numpy(inp["x"].view(np.int16)).view(torch.bfloat16).to(dev)
+    W = torch.from_numpy(inp["W"].view(np.int16)).view(torch.bfloat16).to(dev)
+    b = torch.from_numpy(inp["b"]).to(dev)
+    out = torch.empty((spec.M, spec.N), dtype=torch.bfloat16, device=dev)
+    plan = api.get_plan(spec.M, spec.N, spec.K, "bf16", "bf16", True, spec.ops)
+    info = plan.info()
+
+    def fused():
+        api.linear_epilogue(x, W, b, spec.ops, out=out)
+
+    ms = time_steps(fused, args.steps, args.warmup, torch)
+    flops = spec.flops()
+    tflops = flops / (ms * 1e-3) / 1e12
+    # one launch per step: the average launch duration is the per-step time
+    launch_ms = ms / info["launches"]
+    achieved = flops / (launch_ms * 1e-3) / 1e12
+
+    result = {
+        "metric": "fused GEMM+epilogue TFLOP/s (% of MI355X MFMA peak) vs unfused sequence",
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded: x ~ N(0,1), W, b ~ U(±1/sqrt(8192)))",
+        "config": {"workload": "bf16 GEMM + (x0.5, GELU_tanh, clamp[-1,1]) tail, "
+                               f"x[{spec.M},{spec.K}] W[{spec.N},{spec.K}] -> bf16[{spec.M},{spec.N}]",
+                   "M": spec.M, "N": spec.N, "K": spec.K,
+                   "tile": f"{info['tile_m']}x{info['tile_n']}", "workgroups": info["workgroups"]},
+        "roofline": {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                     "traffic": measured_traffic("fgemm_bf16_gelu_clamp_1024x8192x8192"),
+                     "algorithmic_flops_per_launch": flops,
+                     "algorithmic_bytes_per_launch": spec.bytes()},
+    }
+
+    if not args.no_unfused:
+        bf = b.to(torch.bfloat16)
+
+        def unfused():
+            z = torch.mm(x, W.t())
+            z = z + bf
+            z = z * 0.5
+            z = F.gelu(z, approximate="tanh")
+            return torch.clamp(z, -1.0, 1.0)
+
+        def gemm_only():
+            return torch.mm(x, W.t())
+
+        ms_u = time_steps(unfused, args.steps, args.warmup, torch)
+        ms_g = time_steps(gemm_only, args.steps, args.warmup, torch)
+        result["unfused"] = {"ms": round(ms_u, 5), "tflops": round(flops / (ms_u * 1e-3) / 1e12, 2),
+                             "sequence": "torch.mm (vendor BLAS) -> +b -> *0.5 -> gelu(tanh) -> clamp, bf16"}
+        result["gemm_only"] = {"ms": round(ms_g, 5), "tflops": round(flops / (ms_g * 1e-3) / 1e12, 2)}
+        result["speedup_vs_unfused"] = round(ms_u / ms, 3)
+
+    if not args.no_cpu_baseline:
+        torch.cuda.synchronize()
+        got = out.float().cpu().numpy().astype(np.float64)
+        cpu, rep = cpu_oracle_baseline(spec, inp, args.cpu_seconds, got)
+        result["cpu_baseline"] = cpu
+        result["parity_sample"] = {"rel_err": rep.rel_err, "tol": rep.tol, "ok": bool(rep.ok)}
+
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,215 @@
+/*
+ * fgemm.h — C ABI of the MI355X (gfx950) fused GEMM + epilogue library.
+ *
+ * Two operations are exported:
+ *
+ *  1. fgemm: y = tail(x·Wᵀ + b), a dense GEMM whose post-GEMM ("tail") ops run
+ *     inside the GEMM kernel on the fp32 accumulators, so the matmul result is
+ *     read once and the result written once (paper §IV-B, the four techniques
+ *     found in the generated GEMM + tail-ops kernels: layer-wise fusion,
+ *     mixed-precision execution with fp32 accumulation and post-processing,
+ *     single-pass reductions, partitioning without cross-block reductions).
+ *     The tail is a chain of up to FG_MAX_OPS elementwise ops (scale, add,
+ *     ReLU, GELU-tanh, SiLU, clamp — the pointwise vocabulary of Table III)
+ *     optionally followed by one row reduction: LogSumExp over the N columns
+ *     of each row, or GroupNorm over contiguous channel groups (Table III:
+ *     Scale + LSE, Swish + GroupNorm).
+ *
+ *  2. moe_grouped_ffn: one MoE expert-FFN step of a gpt-oss-20b-like layer
+ *     (paper §IV-A: the MoE decode path and its "MoE finalize" kernel,
+ *     Table I; §V: optimising the whole MoE-MLP block jointly): top-k routing
+ *     over router logits, a stable token permutation by expert, the grouped
+ *     gate/up GEMM with a clamped-SwiGLU epilogue, the grouped down GEMM with
+ *     the routing weight applied in its epilogue, and the finalize sum back to
+ *     token order.
+ *
+ * Conventions shared by every entry point
+ *  - All tensors are row-major and dense. W follows the nn.Linear layout
+ *    [N, K], so both GEMM operands are contiguous along K.
+ *  - Every device buffer is owned by the caller. The library never allocates
+ *    device memory, never synchronises the stream and keeps no pointer after a
+ *    call returns. Work is enqueued on `stream` (a hipStream_t passed as
+ *    void*; NULL is the default stream) and runs asynchronously.
+ *  - Every argument is validated before anything is enqueued. On any error
+ *    nothing is launched and a status other than FG_OK is returned;
+ *    fg_last_error() then holds a one-line description (per thread).
+ *    Launch failures reported by the HIP runtime map to FG_ERR_HIP.
+ *  - Device pointers must be 16-byte aligned. Scalars marked "host" are read
+ *    on the host; everything else is a device pointer.
+ *  - No C++ exception crosses this interface.
+ */
+#ifndef FGEMM_H
+#define FGEMM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  FG_OK = 0,
+  FG_ERR_INVALID_ARG = 1,   /* null pointer, bad shape, bad enum value */
+  FG_ERR_UNSUPPORTED = 2,   /* valid request this build has no kernel for */
+  FG_ERR_ALIGNMENT = 3,     /* pointer or leading dimension not aligned */
+  FG_ERR_WORKSPACE = 4,     /* workspace missing or smaller than required */
+  FG_ERR_HIP = 5            /* the HIP runtime reported a launch error */
+} fg_status;
+
+typedef enum { FG_F32 = 0, FG_BF16 = 1, FG_E4M3 = 2 } fg_dtype;
+
+/* Elementwise tail ops, applied in order to z = x·Wᵀ (+ b), in fp32. */
+typedef enum {
+  FG_OP_SCALE = 0,      /* z·a */
+  FG_OP_ADD = 1,        /* z + a */
+  FG_OP_RELU = 2,       /* max(z, 0) */
+  FG_OP_GELU_TANH = 3,  /* ½z(1 + tanh(√(2/π)(z + 0.044715 z³))) */
+  FG_OP_SILU = 4,       /* z/(1 + e^−z) */
+  FG_OP_CLAMP = 5       /* min(max(z, a), b); requires a ≤ b */
+} fg_op_kind;
+
+typedef struct {
+  int32_t kind;         /* fg_op_kind */
+  float a;
+  float b;
+} fg_op;
+
+typedef enum {
+  FG_RED_NONE = 0,
+  FG_RED_LOGSUMEXP_ROW = 1, /* out[m] = log Σ_n exp(t[m,n]); out is fp32 [M] */
+  FG_RED_GROUPNORM = 2      /* per row, over gn_groups contiguous channel
+                               groups: (t − μ)/√(σ² + eps)·γ[n] + β[n], σ²
+                               biased; out is [M, N] */
+} fg_reduction;
+
+#define FG_MAX_OPS 8
+
+typedef struct {
+  int32_t has_bias;         /* 1: add bias[N] (fp32) before the ops */
+  int32_t n_ops;            /* 0 .. FG_MAX_OPS */
+  fg_op ops[FG_MAX_OPS];
+  int32_t reduction;        /* fg_reduction */
+  int32_t gn_groups;        /* GroupNorm only: N must be a multiple */
+  float gn_eps;             /* GroupNorm only: ≥ 0 */
+} fg_epilogue;
+
+typedef struct fg_plan fg_plan; /* opaque, host memory, immutable once built */
+
+/*
+ * fgemm_plan — validate a problem and choose its kernel (host only; makes no
+ * HIP call, so it can run without a GPU).
+ *   plan     out: receives a new plan, to be released with fgemm_destroy.
+ *   M, N, K  x is [M, K], W is [N, K], output [M, N] (or [M] for LSE).
+ *            M = 0 is a valid empty problem (fgemm_run enqueues nothing);
+ *            K = 0 gives z = b. Each must be < 2^31.
+ *   in_dtype FG_F32 or FG_BF16 for both x and W. K must be a multiple of 4
+ *            (f32) or 8 (bf16) so that rows stay 16-byte aligned
+ *            (FG_ERR_ALIGNMENT otherwise).
+ *   out_dtype FG_F32 or FG_BF16; LogSumExp requires FG_F32. N must be a
+ *            multiple of 4 (f32 out) or 8 (bf16 out) (FG_ERR_ALIGNMENT).
+ *   epi      the tail (copied into the plan; the caller keeps ownership).
+ *            GroupNorm is supported for group widths N/gn_groups of 64 or
+ *            128 channels (FG_ERR_UNSUPPORTED otherwise).
+ */
+fg_status fgemm_plan(fg_plan **plan, int64_t M, int64_t N, int64_t K,
+                     int32_t in_dtype, int32_t out_dtype, const fg_epilogue *epi);
+
+/* Bytes of device workspace fgemm_run needs (the LogSumExp per-tile
+ * (max, Σexp) partials; 0 for the other tails). 0 for a NULL plan. */
+size_t fgemm_workspace_bytes(const fg_plan *plan);
+
+/*
+ * fgemm_run — enqueue y = tail(x·Wᵀ + b) on `stream`.
+ *   A      [M, K] in_dtype.      W      [N, K] in_dtype (both may be NULL when K = 0).
+ *   bias   [N] fp32, required iff epi.has_bias (else ignored, may be NULL).
+ *   gamma, beta  [N] fp32, required iff GroupNorm (else ignored).
+ *   out    [M, N] out_dtype, or [M] fp32 for LogSumExp.
+ *   workspace, ws_bytes  device scratch of at least fgemm_workspace_bytes;
+ *          may be NULL when that is 0. Contents on entry are ignored.
+ * Re-entrant: one plan may be run concurrently on several streams provided
+ * each run has its own output and workspace.
+ */
+fg_status fgemm_run(const fg_plan *plan, const void *A, const void *W,
+                    const float *bias, const float *gamma, const float *beta,
+                    void *out, void *workspace, size_t ws_bytes, void *stream);
+
+void fgemm_destroy(fg_plan *plan);
+
+/* Kernel choice of a plan, for tests and reports: tile rows and columns,
+ * workgroups per launch, and launches per run. Returns FG_ERR_INVALID_ARG
+ * for a NULL plan. Any output pointer may be NULL. */
+fg_status fgemm_plan_info(const fg_plan *plan, int32_t *tile_m, int32_t *tile_n,
+                          int64_t *workgroups, int32_t *launches);
+
+/* ---------------------------------------------------------------------- */
+/* MoE expert FFN                                                         */
+
+typedef struct {
+  int64_t T;                /* tokens (0 allowed: nothing is enqueued) */
+  int64_t H;                /* hidden size; multiple of 64 */
+  int64_t I;                /* expert intermediate size; multiple of 64 */
+  int32_t E;                /* experts, 1 .. 256 */
+  int32_t top_k;            /* experts per token, 1 .. min(E, 8) */
+  int32_t w_dtype;          /* FG_BF16, or FG_E4M3 (W8A8: tokens and the
+                               intermediate are quantised per row on the fly) */
+  float swiglu_alpha;       /* σ(α·gate); gpt-oss uses 1.702 */
+  float swiglu_limit;       /* gate ≤ limit, −limit ≤ up ≤ limit; 7.0 */
+  int32_t gateup_interleaved; /* 0: rows [0, I) gate, [I, 2I) up;
+                                 1: even rows gate, odd rows up */
+} moe_desc;
+
+/* Device workspace moe_grouped_ffn needs for `d` (the permuted
+ * intermediate, per-slot outputs, routing scratch, quantised activations).
+ * 0 if d is NULL or invalid. */
+size_t moe_workspace_bytes(const moe_desc *d);
+
+/*
+ * moe_grouped_ffn — enqueue one MoE expert-FFN step on `stream`.
+ *   tokens         [T, H] bf16.
+ *   router_logits  [T, E] fp32.
+ *   w_gateup       [E, 2I, H] bf16, or e4m3 codes (one byte each).
+ *   w_down         [E, H, I] bf16, or e4m3 codes.
+ *   s_gateup       [E, 2I] fp32 per-row weight scales (e4m3 only, else NULL).
+ *   s_down         [E, H] fp32 per-row weight scales (e4m3 only, else NULL).
+ *   out            [T, H] bf16: out[t] = Σ_j w[t,j]·FFN_{idx[t,j]}(tokens[t]).
+ *   topk_idx       [T, top_k] int32 out: selected experts, logits descending,
+ *                  ties to the lower expert index.
+ *   topk_w         [T, top_k] fp32 out: softmax over the selected logits.
+ *   perm           [T·top_k] int32 out: slot ids p = t·top_k + j sorted by
+ *                  (expert, p) — stable, hence unique.
+ *   expert_offsets [E + 1] int32 out: exclusive prefix of the per-expert
+ *                  slot counts; expert e owns perm[offsets[e] .. offsets[e+1]).
+ *   workspace, ws_bytes  at least moe_workspace_bytes(d).
+ * Nothing is copied back to the host: the per-expert counts stay on the
+ * device and the grouped GEMMs read them there.
+ */
+fg_status moe_grouped_ffn(const moe_desc *d, const void *tokens,
+                          const float *router_logits, const void *w_gateup,
+                          const void *w_down, const float *s_gateup,
+                          const float *s_down, void *out, int32_t *topk_idx,
+                          float *topk_w, int32_t *perm, int32_t *expert_offsets,
+                          void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * fg_quantize_rows_e4m3 — the W8A8 path's activation quantiser as a
+ * standalone call: for each of `rows` rows of `cols` bf16 values,
+ * s = amax/448 (1 for an all-zero row) and q = e4m3fn(v/s) with
+ * round-to-nearest-even and saturation to ±448; both decisions in fp32.
+ *   x [rows, cols] bf16; q [rows, cols] uint8 codes out; s [rows] fp32 out.
+ *   cols must be a multiple of 8.
+ */
+fg_status fg_quantize_rows_e4m3(const void *x, int64_t rows, int64_t cols,
+                                uint8_t *q, float *s, void *stream);
+
+/* Static description of a status code. */
+const char *fg_status_str(fg_status s);
+
+/* Description of the last error returned on the calling thread ("" if none). */
+const char *fg_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FGEMM_H */

@@ -1,0 +1,219 @@
+// fg_epilogue.hpp — the in-register tail applied to fp32 accumulator tiles.
+//
+// The post-GEMM sequence runs on the accumulators before the single store
+// (paper §IV-B, layer-wise fusion and fp32 post-processing). Elementwise ops
+// are applied one op at a time over the whole tile, so the branch on the op
+// kind is uniform across the workgroup. Row reductions follow the
+// single-pass pattern of §IV-B: GroupNorm groups never straddle a tile, so
+// mean and variance come from the registers plus one exchange between the
+// two waves that share a row; LogSumExp spans N tiles, so each tile emits its
+// (max, Σexp) pair and a second, tiny pass combines them with the rescaling
+// identity of online softmax (§I).
+#pragma once
+
+#include <math.h>
+
+#include "fg_tile.hpp"
+#include "fgemm.h"
+
+namespace fg {
+
+struct EpiArgs {
+  int32_t n_ops;
+  int32_t kind[FG_MAX_OPS];
+  float a[FG_MAX_OPS];
+  float b[FG_MAX_OPS];
+};
+
+// GELU, tanh form: ½u(1 + tanh(√(2/π)(u + 0.044715u³))).
+__device__ __forceinline__ float gelu_tanh(float u) {
+  const float k0 = 0.7978845608028654f;  // √(2/π)
+  const float k1 = 0.044715f;
+  return 0.5f * u * (1.0f + tanhf(k0 * (u + k1 * u * u * u)));
+}
+
+// SiLU u·σ(u) = u/(1 + e^−u); for u → −∞ the quotient tends to −0.
+__device__ __forceinline__ float silu(float u) { return u / (1.0f + expf(-u)); }
+
+// The chain runs over one block of FN·4 accumulators at a time (one fm),
+// all ops on that block before the next, so only that block is live in
+// VGPRs next to the transcendental temporaries; the accumulators stay in
+// AGPRs otherwise.
+template <class TL>
+__device__ __forceinline__ void apply_ops(const EpiArgs& ep, f32x4 (&acc)[TL::FM][TL::FN]) {
+  if (ep.n_ops == 0) return;
+#pragma unroll
+  for (int fm = 0; fm < TL::FM; ++fm) {
+    float v[TL::FN * 4];
+#pragma unroll
+    for (int fn = 0; fn < TL::FN; ++fn)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[fn * 4 + i] = acc[fm][fn][i];
+    for (int o = 0; o < ep.n_ops; ++o) {
+      const int kind = ep.kind[o];
+      const float a = ep.a[o], b = ep.b[o];
+#define FG_EACH(EXPR)                                           \
+  _Pragma("unroll") for (int e = 0; e < TL::FN * 4; ++e) {      \
+    const float u = v[e];                                       \
+    v[e] = (EXPR);                                              \
+  }
+      switch (kind) {
+        case FG_OP_SCALE: FG_EACH(u * a) break;
+        case FG_OP_ADD: FG_EACH(u + a) break;
+        case FG_OP_RELU: FG_EACH(fmaxf(u, 0.0f)) break;
+        case FG_OP_GELU_TANH: FG_EACH(gelu_tanh(u)) break;
+        case FG_OP_SILU: FG_EACH(silu(u)) break;
+        case FG_OP_CLAMP: FG_EACH(fminf(fmaxf(u, a), b)) break;
+        default: break;
+      }
+#undef FG_EACH
+    }
+#pragma unroll
+    for (int fn = 0; fn < TL::FN; ++fn)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[fm][fn][i] = v[fn * 4 + i];
+  }
+}
+
+// Add bias[n0 + col] (columns past N read nothing and add 0).
+template <class TL>
+__device__ __forceinline__ void add_bias(const float* bias, int n0, int N, f32x4 (&acc)[TL::FM][TL::FN]) {
+#pragma unroll
+  for (int fn = 0; fn < TL::FN; ++fn) {
+    const int n = n0 + acc_col<TL>(fn);
+    const float bv = n < N ? bias[n] : 0.0f;
+#pragma unroll
+    for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[fm][fn][i] += bv;
+  }
+}
+
+// Per-tile row LogSumExp partials: for every tile row r, over the tile's
+// valid columns, m = max t and s = Σ exp(t − m). `red` needs 2·WN·BM floats
+// of LDS. Rows ≥ M are skipped. ws is [M, tiles_n] (m, s) pairs.
+template <class TL>
+__device__ __forceinline__ void lse_partials(f32x4 (&acc)[TL::FM][TL::FN], float* red, int m0, int n0,
+                                             int M, int N, int tn, int tiles_n, float2* ws) {
+  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int wn = wave % TL::WN;
+  float* rmax = red;
+  float* rsum = red + TL::WN * TL::BM;
+  bool colok[TL::FN];
+#pragma unroll
+  for (int fn = 0; fn < TL::FN; ++fn) colok[fn] = n0 + acc_col<TL>(fn) < N;
+#pragma unroll
+  for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float mx = -INFINITY;
+#pragma unroll
+      for (int fn = 0; fn < TL::FN; ++fn)
+        if (colok[fn]) mx = fmaxf(mx, acc[fm][fn][i]);
+      mx = row16_max(mx);
+      if ((l & 15) == 0) rmax[wn * TL::BM + acc_row<TL>(fm, i)] = mx;
+    }
+  __syncthreads();
+#pragma unroll
+  for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = acc_row<TL>(fm, i);
+      float mx = rmax[r];
+#pragma unroll
+      for (int w = 1; w < TL::WN; ++w) mx = fmaxf(mx, rmax[w * TL::BM + r]);
+      float s = 0.0f;
+#pragma unroll
+      for (int fn = 0; fn < TL::FN; ++fn)
+        if (colok[fn]) s += expf(acc[fm][fn][i] - mx);
+      s = row16_sum(s);
+      if ((l & 15) == 0) rsum[wn * TL::BM + r] = s;
+    }
+  __syncthreads();
+  // one thread per tile row writes the pair
+  for (int r = threadIdx.x; r < TL::BM; r += TL::THREADS) {
+    if (m0 + r >= M) continue;
+    float mx = rmax[r], s = 0.0f;
+#pragma unroll
+    for (int w = 1; w < TL::WN; ++w) mx = fmaxf(mx, rmax[w * TL::BM + r]);
+#pragma unroll
+    for (int w = 0; w < TL::WN; ++w) s += rsum[w * TL::BM + r];
+    ws[(int64_t)(m0 + r) * tiles_n + tn] = make_float2(mx, s);
+  }
+}
+
+// GroupNorm inside the tile. Group width gw is a multiple of the wave tile
+// width TN and divides BN, so each wave's columns lie in one group and a
+// group's statistics are the sum over the waves whose columns it covers.
+// `red` needs WN·BM floats of LDS.
+template <class TL>
+__device__ __forceinline__ void groupnorm_tile(f32x4 (&acc)[TL::FM][TL::FN], float* red, int n0, int N,
+                                               int gw, float eps, const float* gamma, const float* beta) {
+  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const int wn = wave % TL::WN;
+  const int my_group = (wn * TL::TN) / gw;
+  const float inv_gw = 1.0f / (float)gw;
+  float mean[TL::FM][4];
+  // pass 1: mean
+#pragma unroll
+  for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float s = 0.0f;
+#pragma unroll
+      for (int fn = 0; fn < TL::FN; ++fn) s += acc[fm][fn][i];
+      s = row16_sum(s);
+      if ((l & 15) == 0) red[wn * TL::BM + acc_row<TL>(fm, i)] = s;
+    }
+  __syncthreads();
+#pragma unroll
+  for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = acc_row<TL>(fm, i);
+      float s = 0.0f;
+#pragma unroll
+      for (int w = 0; w < TL::WN; ++w)
+        if ((w * TL::TN) / gw == my_group) s += red[w * TL::BM + r];
+      mean[fm][i] = s * inv_gw;
+    }
+  __syncthreads();
+  // pass 2: biased variance about the mean
+#pragma unroll
+  for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float s = 0.0f;
+#pragma unroll
+      for (int fn = 0; fn < TL::FN; ++fn) {
+        const float d = acc[fm][fn][i] - mean[fm][i];
+        s += d * d;
+      }
+      s = row16_sum(s);
+      if ((l & 15) == 0) red[wn * TL::BM + acc_row<TL>(fm, i)] = s;
+    }
+  __syncthreads();
+  float gm[TL::FN], bt[TL::FN];
+#pragma unroll
+  for (int fn = 0; fn < TL::FN; ++fn) {
+    const int n = n0 + acc_col<TL>(fn);
+    gm[fn] = n < N ? gamma[n] : 0.0f;
+    bt[fn] = n < N ? beta[n] : 0.0f;
+  }
+#pragma unroll
+  for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = acc_row<TL>(fm, i);
+      float s = 0.0f;
+#pragma unroll
+      for (int w = 0; w < TL::WN; ++w)
+        if ((w * TL::TN) / gw == my_group) s += red[w * TL::BM + r];
+      const float rstd = 1.0f / sqrtf(s * inv_gw + eps);
+#pragma unroll
+      for (int fn = 0; fn < TL::FN; ++fn)
+        acc[fm][fn][i] = (acc[fm][fn][i] - mean[fm][i]) * rstd * gm[fn] + bt[fn];
+    }
+}
+
+}  // namespace fg

@@ -1,0 +1,39 @@
+"""Shared helpers of the GPU parity tests: move seeded inputs to the device,
+run the library, bring results back as fp64 for the oracle comparison."""
+
+import numpy as np
+import torch
+
+from oracle import bf16_decode
+
+
+def require_gpu():
+    import pytest
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+
+
+def dev_bf16(bits):
+    """uint16 bf16 bit patterns -> device bfloat16 tensor (same bits)."""
+    t = torch.from_numpy(np.ascontiguousarray(bits).view(np.int16))
+    return t.view(torch.bfloat16).cuda()
+
+
+def dev_f32(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
+
+
+def dev_u8(a):
+    return torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint8)).cuda()
+
+
+def host64(t):
+    """Device tensor -> fp64 numpy (bf16 decoded exactly)."""
+    t = t.detach().cpu()
+    if t.dtype == torch.bfloat16:
+        return bf16_decode(t.view(torch.int16).numpy().view(np.uint16))
+    return t.numpy().astype(np.float64)
+
+
+def log(msg):
+    print(msg, flush=True)

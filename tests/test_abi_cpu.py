@@ -1,0 +1,146 @@
+"""Host-side checks of the C ABI (no GPU needed).
+
+The library loads without a GPU, exports every function ``include/fgemm.h``
+declares, and its validation rejects bad requests with the documented status
+before any HIP call: fgemm_plan is host-only, and fgemm_run /
+moe_grouped_ffn / fg_quantize_rows_e4m3 return on invalid arguments before
+enqueueing anything."""
+
+import ctypes as C
+import os
+import re
+
+import pytest
+
+from paper_2606_02963_amd import _lib as L
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "fgemm.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_]\w*\s*\**\s*([A-Za-z_]\w*)\s*\(", text, flags=re.M)
+    return sorted(set(n for n in names if n not in ("if", "while")))
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for want in ("fgemm_plan", "fgemm_run", "fgemm_destroy", "fgemm_workspace_bytes",
+                 "moe_grouped_ffn", "moe_workspace_bytes", "fg_status_str", "fg_last_error"):
+        assert want in names
+
+
+def test_library_exports_every_declared_symbol():
+    lib = C.CDLL(L.LIB_PATH)
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+
+
+def E(**kw):
+    return L.make_epilogue(**kw)
+
+
+def plan_status(M, N, K, i, o, epi):
+    try:
+        L.fgemm_plan(M, N, K, i, o, epi)
+        return L.FG_OK
+    except L.FgError as e:
+        return e.status
+
+
+def test_plan_validation_statuses():
+    ok = E(has_bias=True, ops=(("relu",), ("scale", 2.0)))
+    assert plan_status(128, 256, 256, "f32", "f32", ok) == L.FG_OK
+    assert plan_status(0, 256, 256, "bf16", "bf16", ok) == L.FG_OK          # empty problem is valid
+    assert plan_status(8, 256, 0, "bf16", "bf16", ok) == L.FG_OK            # K = 0: z = b
+    assert plan_status(-1, 256, 256, "bf16", "bf16", ok) == L.FG_ERR_INVALID_ARG
+    assert plan_status(8, 0, 256, "bf16", "bf16", ok) == L.FG_ERR_INVALID_ARG
+    assert plan_status(8, 256, 2 ** 31, "bf16", "bf16", ok) == L.FG_ERR_INVALID_ARG
+    assert plan_status(8, 256, 260, "bf16", "bf16", ok) == L.FG_ERR_ALIGNMENT  # K % 8
+    assert plan_status(8, 256, 258, "f32", "f32", ok) == L.FG_ERR_ALIGNMENT    # K % 4
+    assert plan_status(8, 252, 256, "bf16", "bf16", ok) == L.FG_ERR_ALIGNMENT  # N % 8 (bf16 out)
+    assert plan_status(8, 256, 256, "e4m3", "bf16", ok) == L.FG_ERR_UNSUPPORTED
+    assert plan_status(8, 256, 256, 7, "bf16", ok) == L.FG_ERR_INVALID_ARG
+    assert plan_status(8, 256, 256, "bf16", 9, ok) == L.FG_ERR_INVALID_ARG
+    assert plan_status(8, 256, 256, "bf16", "bf16", None) == L.FG_ERR_INVALID_ARG
+    bad_kind = E(ops=((17, 0.0),))
+    assert plan_status(8, 256, 256, "bf16", "bf16", bad_kind) == L.FG_ERR_INVALID_ARG
+    bad_clamp = E(ops=(("clamp", 1.0, -1.0),))
+    assert plan_status(8, 256, 256, "bf16", "bf16", bad_clamp) == L.FG_ERR_INVALID_ARG
+    nan_op = E(ops=(("scale", float("nan")),))
+    assert plan_status(8, 256, 256, "bf16", "bf16", nan_op) == L.FG_ERR_INVALID_ARG
+    e = E(ops=(("relu",),))
+    e.n_ops = 9
+    assert plan_status(8, 256, 256, "bf16", "bf16", e) == L.FG_ERR_INVALID_ARG
+    lse = E(reduction="lse")
+    assert plan_status(8, 100, 256, "bf16", "f32", lse) == L.FG_OK          # any N for a row LSE
+    assert plan_status(8, 256, 256, "bf16", "bf16", lse) == L.FG_ERR_INVALID_ARG
+    gn = dict(reduction="groupnorm", gn_groups=32, gn_eps=1e-5)
+    assert plan_status(8, 4096, 256, "bf16", "bf16", E(**gn)) == L.FG_OK      # width 128
+    assert plan_status(8, 2048, 256, "bf16", "bf16", E(**gn)) == L.FG_OK      # width 64
+    assert plan_status(8, 1024, 256, "bf16", "bf16", E(**gn)) == L.FG_ERR_UNSUPPORTED  # width 32
+    assert plan_status(8, 4008, 256, "bf16", "bf16", E(**gn)) == L.FG_ERR_INVALID_ARG  # not divisible
+    gn_neg = E(reduction="groupnorm", gn_groups=32, gn_eps=-1.0)
+    assert plan_status(8, 4096, 256, "bf16", "bf16", gn_neg) == L.FG_ERR_INVALID_ARG
+
+
+def test_last_error_describes_the_failure():
+    with pytest.raises(L.FgError) as ei:
+        L.fgemm_plan(8, 256, 260, "bf16", "bf16", E())
+    assert "K=260" in str(ei.value) and "multiple of 8" in L.last_error()
+
+
+def test_tile_choice_and_workspace():
+    p = L.fgemm_plan(1024, 8192, 8192, "bf16", "bf16", E(has_bias=True))
+    assert p.info() == {"tile_m": 256, "tile_n": 128, "workgroups": 256, "launches": 1}
+    assert p.workspace_bytes() == 0
+    p = L.fgemm_plan(300, 520, 264, "bf16", "bf16", E())
+    assert p.info()["tile_m"] == 128 and p.info()["workgroups"] == 3 * 5
+    p = L.fgemm_plan(4096, 8192, 4096, "bf16", "f32", E(reduction="lse"))
+    assert p.info()["launches"] == 2
+    assert p.workspace_bytes() == 4096 * 64 * 8
+    p = L.fgemm_plan(0, 8192, 4096, "bf16", "bf16", E())
+    assert p.info()["workgroups"] == 0 and p.info()["launches"] == 0
+    p = L.fgemm_plan(128, 256, 256, "f32", "f32", E())
+    assert (p.info()["tile_m"], p.info()["tile_n"]) == (64, 128)
+
+
+def test_run_validation_enqueues_nothing():
+    p = L.fgemm_plan(64, 256, 256, "bf16", "bf16", E(has_bias=True))
+    fake = 1 << 40          # never dereferenced: validation fails first
+    with pytest.raises(L.FgError) as ei:
+        L.fgemm_run(p, None, fake, fake, None, None, fake, None, 0)
+    assert ei.value.status == L.FG_ERR_INVALID_ARG
+    with pytest.raises(L.FgError) as ei:
+        L.fgemm_run(p, fake, fake, None, None, None, fake, None, 0)       # bias missing
+    assert ei.value.status == L.FG_ERR_INVALID_ARG
+    with pytest.raises(L.FgError) as ei:
+        L.fgemm_run(p, fake + 2, fake, fake, None, None, fake, None, 0)   # misaligned A
+    assert ei.value.status == L.FG_ERR_ALIGNMENT
+    lse = L.fgemm_plan(64, 256, 256, "bf16", "f32", E(reduction="lse"))
+    with pytest.raises(L.FgError) as ei:
+        L.fgemm_run(lse, fake, fake, None, None, None, fake, fake, 8)     # workspace too small
+    assert ei.value.status == L.FG_ERR_WORKSPACE
+    gn = L.fgemm_plan(64, 256, 256, "bf16", "bf16", E(reduction="groupnorm", gn_groups=2))
+    with pytest.raises(L.FgError) as ei:
+        L.fgemm_run(gn, fake, fake, None, None, None, fake, None, 0)      # gamma/beta missing
+    assert ei.value.status == L.FG_ERR_INVALID_ARG
+    empty = L.fgemm_plan(0, 256, 256, "bf16", "bf16", E())
+    L.fgemm_run(empty, None, None, None, None, None, None, None, 0)       # M = 0: nothing to do
+
+
+def test_quantize_validation():
+    with pytest.raises(L.FgError) as ei:
+        L.fg_quantize_rows_e4m3(1 << 40, 4, 12, 1 << 40, 1 << 40)
+    assert ei.value.status == L.FG_ERR_ALIGNMENT
+    with pytest.raises(L.FgError) as ei:
+        L.fg_quantize_rows_e4m3(None, 4, 16, 1 << 40, 1 << 40)
+    assert ei.value.status == L.FG_ERR_INVALID_ARG
+    L.fg_quantize_rows_e4m3(None, 0, 16, None, None)                       # zero rows: no-op
+
+
+def test_status_strings():
+    for st in range(6):
+        assert L.status_str(st).startswith("FG_")
+    assert "unknown" in L.status_str(42)
