@@ -34,7 +34,9 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--warmup-seconds", type=float, default=1.0,
+                    help="extra untimed work first, so clocks settle before timing")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample time")
@@ -61,6 +63,15 @@ def measured_traffic(name):
     if d.get("kernel_source_hash") != kernel_source_hash():
         return None
     return d.get("hbm_bytes_per_launch")
+
+
+def settle(fn, seconds, torch):
+    """Run untimed work for about `seconds` so the clocks reach steady state."""
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(10):
+            fn()
+        torch.cuda.synchronize()
 
 
 def time_steps(fn, steps, warmup, torch):
@@ -143,6 +154,7 @@ def main():
     def fused():
         api.linear_epilogue(x, W, b, spec.ops, out=out)
 
+    settle(fused, args.warmup_seconds, torch)
     ms = time_steps(fused, args.steps, args.warmup, torch)
     flops = spec.flops()
     tflops = flops / (ms * 1e-3) / 1e12

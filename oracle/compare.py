@@ -23,7 +23,10 @@ import numpy as np
 TOL = {"f32": 1e-4, "bf16": 1e-2, "e4m3": 4e-2}
 
 
-def rel_err(y, r):
+def rel_err(y, r, slack=None):
+    """RMS-floored max relative error. ``slack`` (optional, same shape):
+    per-element absolute deviation that is known to be legitimate (a
+    rounding decision either way is correct) and is subtracted first."""
     y = np.asarray(y, dtype=np.float64).ravel()
     r = np.asarray(r, dtype=np.float64).ravel()
     if y.shape != r.shape:
@@ -34,7 +37,10 @@ def rel_err(y, r):
         return float("inf")
     rms = float(np.sqrt(np.mean(r * r)))
     floor = np.maximum(np.abs(r), rms if rms > 0 else 1.0)
-    return float(np.max(np.abs(y - r) / floor))
+    d = np.abs(y - r)
+    if slack is not None:
+        d = np.maximum(d - np.asarray(slack, dtype=np.float64).ravel(), 0.0)
+    return float(np.max(d / floor))
 
 
 @dataclass
@@ -53,8 +59,9 @@ class ComparisonReport:
                 f"normwise={self.normwise:.3e} max_abs={self.max_abs:.3e}")
 
 
-def compare(y, r, dtype):
-    """Full report: the pass metric plus the normwise max|y−r|/max|r|."""
+def compare(y, r, dtype, slack=None):
+    """Full report: the pass metric (after the optional legitimate-deviation
+    slack) plus the normwise max|y−r|/max|r| (without it)."""
     y = np.asarray(y, dtype=np.float64)
     r = np.asarray(r, dtype=np.float64)
     if y.shape != r.shape:
@@ -62,5 +69,5 @@ def compare(y, r, dtype):
     d = np.abs(y - r)
     mx = float(np.max(np.abs(r))) if r.size else 0.0
     max_abs = float(np.max(d)) if d.size else 0.0
-    return ComparisonReport(rel_err(y, r), max_abs / mx if mx else max_abs,
+    return ComparisonReport(rel_err(y, r, slack), max_abs / mx if mx else max_abs,
                             max_abs, TOL[dtype])

@@ -23,16 +23,18 @@ The oracle takes the block's steps in order, each as its plain definition:
   expert e  X = x[perm[r] // k] for the rows r of expert e;
             G = X·W_gu[e]ᵀ, gate | up = the two halves of G (or its even /
             odd columns when interleaved); h = clamped SwiGLU(gate, up);
-            h is stored in the method's declared intermediate format
-            (bf16 RNE, or e4m3 with a per-row fp32 scale), modelled here;
+            h is stored in the method's declared intermediate format,
+            modelled here: bf16 RNE; in the W8A8 variant the bf16 h is
+            then quantised per row to e4m3 with an fp32 scale;
             y_slot[rows] = h·W_d[e]ᵀ
   finalize  out[t] = Σ_j w[t, j]·y_slot[t·k + j], j ascending
 
 fp8 (W8A8) variant: weights are stored as e4m3 codes with one fp32 scale per
 output row (decoded before they reach this oracle); activations (x per
-token, h per slot row) are quantised online with s = amax/448 and
-code = RNE_sat(v / s). Those quantisation decisions are taken in fp32, the
-precision the kernel takes them in, so both sides pick the same code.
+token, and the bf16-stored h per slot row) are quantised online with
+s = amax/448 and code = RNE_sat(v / s). Those quantisation decisions are
+taken in fp32 on the stored (bf16) values, the precision the kernel takes
+them in, so both sides pick the same code for the same stored value.
 """
 
 import numpy as np
@@ -93,6 +95,49 @@ def _dequant_rows(codes, s):
     return e4m3_decode(codes) * np.asarray(s, dtype=np.float64)[..., None]
 
 
+def _dequant_with_scale(b, s):
+    """e4m3 code of fp32(b/s) (RNE, saturated) decoded and rescaled, per row scale s."""
+    s = np.asarray(s, dtype=np.float64)[..., None]
+    return e4m3_decode(e4m3_encode_rne_sat(f32_round(f32_round(b) / s))) * s
+
+
+def _bf16(v):
+    return bf16_decode(bf16_encode_rne(v))
+
+
+# Relative and row-absolute size of the neighbourhood of a storage rounding
+# boundary inside which a kernel that evaluates h in fp32 (a different
+# rounding order than this fp64 oracle) may legitimately take the other
+# rounding decision. Both are far above fp32 evaluation error of h and far
+# below any tolerance.
+FRAGILE_REL = 2.0 ** -16
+FRAGILE_ABS = 2.0 ** -20
+
+
+def storage_deviation(h, storage):
+    """Largest change of the stored value of each element of h (per row for
+    the per-row-scaled e4m3 storage) over the rounding decisions that are
+    within FRAGILE_REL·|h| + FRAGILE_ABS·max|h_row| of a boundary. Zero for
+    every element whose stored value is robust. Returns (stored, deviation)."""
+    h = np.asarray(h, dtype=np.float64)
+    pert = FRAGILE_REL * np.abs(h) + FRAGILE_ABS * np.max(np.abs(h), axis=-1, keepdims=True)
+    if storage == "none":
+        return h, np.zeros_like(h)
+    b_ref, b_lo, b_hi = _bf16(h), _bf16(h - pert), _bf16(h + pert)
+    if storage == "bf16":
+        return b_ref, np.maximum(np.abs(b_lo - b_ref), np.abs(b_hi - b_ref))
+    if storage != "e4m3":
+        raise ValueError(f"unknown storage {storage!r}")
+    q, s_ref = ref_quant_rows_e4m3(b_ref)
+    stored = _dequant_rows(q, s_ref)
+    scales = [s_ref, ref_quant_rows_e4m3(b_lo)[1], ref_quant_rows_e4m3(b_hi)[1]]
+    dev = np.zeros_like(h)
+    for b in (b_ref, b_lo, b_hi):
+        for sc in scales:
+            dev = np.maximum(dev, np.abs(_dequant_with_scale(b, sc) - stored))
+    return stored, dev
+
+
 def _split_gate_up(G, I, interleaved):
     if interleaved:
         return G[:, 0::2], G[:, 1::2]
@@ -100,10 +145,11 @@ def _split_gate_up(G, I, interleaved):
 
 
 def ref_expert_rows(X, W_gu, W_d, storage="bf16", act_quant=False, alpha=1.702,
-                    limit=7.0, interleaved=False):
+                    limit=7.0, interleaved=False, with_bound=False):
     """One expert's FFN over rows X [n, H] → y [n, H] (unweighted), fp64.
 
-    storage: "bf16" or "e4m3" — the declared format of the intermediate h.
+    storage: the declared format of the intermediate h — "bf16" (RNE),
+    "e4m3" (bf16 RNE, then per-row e4m3 with an fp32 scale) or "none".
     act_quant: quantise X per row to e4m3 first (the W8A8 variant)."""
     X = np.asarray(X, dtype=np.float64)
     I = W_d.shape[1]
@@ -113,18 +159,22 @@ def ref_expert_rows(X, W_gu, W_d, storage="bf16", act_quant=False, alpha=1.702,
     G = X @ np.asarray(W_gu, dtype=np.float64).T
     gate, up = _split_gate_up(G, I, interleaved)
     h = ref_swiglu_clamped(gate, up, alpha, limit)
+    W_d = np.asarray(W_d, dtype=np.float64)
+    if with_bound:
+        h, dev = storage_deviation(h, storage)
+        return h @ W_d.T, dev @ np.abs(W_d).T
     if storage == "bf16":
         h = bf16_decode(bf16_encode_rne(h))
     elif storage == "e4m3":
-        q, s = ref_quant_rows_e4m3(h)
+        q, s = ref_quant_rows_e4m3(bf16_decode(bf16_encode_rne(h)))
         h = _dequant_rows(q, s)
     elif storage != "none":
         raise ValueError(f"unknown storage {storage!r}")
-    return h @ np.asarray(W_d, dtype=np.float64).T
+    return h @ W_d.T
 
 
 def ref_moe(x, logits, weights, k, storage="bf16", act_quant=False, alpha=1.702,
-            limit=7.0, interleaved=False, tokens=None):
+            limit=7.0, interleaved=False, tokens=None, with_bound=False):
     """The MoE expert FFN step, fp64.
 
     x: [T, H] fp64 (decoded bf16 tokens); logits: [T, E] (fp32 values);
@@ -132,7 +182,13 @@ def ref_moe(x, logits, weights, k, storage="bf16", act_quant=False, alpha=1.702,
     applied), or a pair of arrays [E, 2I, H], [E, H, I].
     tokens: optional subset of token ids whose outputs to compute (a token's
     output depends only on its own row and its own routing).
-    Returns a dict: out [T or len(tokens), H], idx, w, counts, offsets, perm.
+    with_bound: also return "out_bound", per output element the largest
+    change any storage-rounding decision of h within the fragile
+    neighbourhood of a boundary (see storage_deviation) can cause; a kernel
+    that evaluates h in another rounding order may take those decisions
+    either way, and every such result is correct.
+    Returns a dict: out [T or len(tokens), H], idx, w, counts, offsets, perm
+    (and out_bound).
     """
     x = np.asarray(x, dtype=np.float64)
     T, H = x.shape
@@ -147,18 +203,30 @@ def ref_moe(x, logits, weights, k, storage="bf16", act_quant=False, alpha=1.702,
     row_of_token = np.full(T, -1, dtype=np.int64)
     row_of_token[tok] = np.arange(tok.size)
     y_slot = np.zeros((tok.size * k, H), dtype=np.float64)
+    b_slot = np.zeros((tok.size * k, H), dtype=np.float64) if with_bound else None
     for e in range(E):
         slots = perm[offsets[e]:offsets[e + 1]].astype(np.int64)
         slots = slots[row_of_token[slots // k] >= 0]
         if slots.size == 0:
             continue
         W_gu, W_d = weights(e)
-        y = ref_expert_rows(x[slots // k], W_gu, W_d, storage, act_quant, alpha,
-                            limit, interleaved)
-        y_slot[row_of_token[slots // k] * k + slots % k] = y
+        dst = row_of_token[slots // k] * k + slots % k
+        if with_bound:
+            y, yb = ref_expert_rows(x[slots // k], W_gu, W_d, storage, act_quant, alpha,
+                                    limit, interleaved, with_bound=True)
+            b_slot[dst] = yb
+        else:
+            y = ref_expert_rows(x[slots // k], W_gu, W_d, storage, act_quant, alpha,
+                                limit, interleaved)
+        y_slot[dst] = y
     # finalize: routing-weighted sum over the k slots of each token, j ascending
     out = np.zeros((tok.size, H), dtype=np.float64)
+    bound = np.zeros((tok.size, H), dtype=np.float64) if with_bound else None
     for j in range(k):
         out += w[tok, j][:, None] * y_slot[j::k]
-    return {"out": out, "idx": idx, "w": w, "counts": counts,
-            "offsets": offsets, "perm": perm}
+        if with_bound:
+            bound += w[tok, j][:, None] * b_slot[j::k]
+    res = {"out": out, "idx": idx, "w": w, "counts": counts, "offsets": offsets, "perm": perm}
+    if with_bound:
+        res["out_bound"] = bound
+    return res

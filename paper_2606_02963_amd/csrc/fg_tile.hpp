@@ -1,7 +1,6 @@
 // fg_tile.hpp — the tiled MFMA main loop shared by every GEMM in the library.
 //
-// One workgroup of 256 threads (4 wave64s, 2 × 2) computes a BM × BN tile of
-// acc = A·Bᵀ, where A rows and B rows are both contiguous along K (x rows and
+// One workgroup of WM × WN wave64s computes a BM × BN tile of acc = A·Bᵀ, where A rows and B rows are both contiguous along K (x rows and
 // nn.Linear weight rows). Per K stage each tile row contributes 128 bytes
 // (8 chunks of 16 B): 32 fp32, 64 bf16 or 128 e4m3 values. Stages are staged
 // HBM → VGPR → LDS with 128-bit loads and stores and double-buffered in LDS,
@@ -40,11 +39,12 @@ template <> struct InTraits<In::F32>  { static constexpr int EPC = 4,  ESIZE = 4
 template <> struct InTraits<In::BF16> { static constexpr int EPC = 8,  ESIZE = 2; };
 template <> struct InTraits<In::E4M3> { static constexpr int EPC = 16, ESIZE = 1; };
 
-template <In IN_, int BM_, int BN_>
+template <In IN_, int BM_, int BN_, int WM_ = 2, int WN_ = 2>
 struct Tile {
   static constexpr In IN = IN_;
   static constexpr int BM = BM_, BN = BN_;
-  static constexpr int THREADS = 256, WM = 2, WN = 2;
+  static constexpr int WM = WM_, WN = WN_, NWAVES = WM * WN, THREADS = 64 * NWAVES;
+  static constexpr int RSTRIDE = THREADS / 8;          // rows between a thread's successive loads
   static constexpr int TM = BM / WM, TN = BN / WN;     // wave tile
   static constexpr int FM = TM / 16, FN = TN / 16;     // 16×16 fragments per wave
   static constexpr int ROWB = 128;                      // bytes per tile row per stage
@@ -55,7 +55,8 @@ struct Tile {
   static constexpr int B_LD = BN * 8 / THREADS;
   static constexpr int STAGE_BYTES = (BM + BN) * ROWB;
   static constexpr int LOOP_LDS = 2 * STAGE_BYTES;
-  static_assert(BM % 32 == 0 && BN % 32 == 0, "tile sides must be multiples of 32");
+  static_assert(BM % RSTRIDE == 0 && BN % RSTRIDE == 0, "tile sides must be multiples of THREADS/8");
+  static_assert(TM % 16 == 0 && TN % 16 == 0, "wave tiles must be multiples of 16");
 };
 
 __device__ __forceinline__ int lds_off(int row, int chunk) {
@@ -63,7 +64,7 @@ __device__ __forceinline__ int lds_off(int row, int chunk) {
 }
 
 // Row sources for the stage loads. Thread t owns tile rows
-// (t >> 3) + 32·p, p < NLD; `ptr[p]` is the start of that row in global
+// (t >> 3) + (THREADS/8)·p, p < NLD; `ptr[p]` is the start of that row in global
 // memory. Rows past the matrix edge point at any valid row: their LDS copy
 // only feeds accumulator rows / columns that are never stored.
 template <int NLD>
@@ -73,17 +74,17 @@ struct RowSet {
 
 // Direct HBM → LDS load of one full stage (every row has 128 valid bytes at
 // kbyte): global_load_lds_dwordx4 writes lane i's 16 bytes at LDS offset
-// 16·i of a wave-uniform 1 KiB block, i.e. block b = wave + 4p holds tile
-// rows 8b .. 8b + 7 with physical chunk i & 7. The lane therefore fetches
-// logical chunk (i & 7) ^ (i >> 3), the inverse of the LDS swizzle.
-template <int NLD>
+// 16·i of a wave-uniform 1 KiB block, i.e. block b = wave + NWAVES·p holds
+// tile rows 8b .. 8b + 7 with physical chunk i & 7. The lane therefore
+// fetches logical chunk (i & 7) ^ (i >> 3), the inverse of the LDS swizzle.
+template <int NWAVES, int NLD>
 __device__ __forceinline__ void load_stage_direct(const RowSet<NLD>& rs, int64_t kbyte, char* sbase) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int c = (lane & 7) ^ (lane >> 3);
 #pragma unroll
   for (int p = 0; p < NLD; ++p) {
     const char* src = rs.ptr[p] + kbyte + c * 16;
-    char* dst = sbase + (wave + 4 * p) * 1024;
+    char* dst = sbase + (wave + NWAVES * p) * 1024;
     __builtin_amdgcn_global_load_lds(static_cast<const void*>(src),
                                      (__attribute__((address_space(3))) void*)(dst), 16, 0, 0);
   }
@@ -91,7 +92,7 @@ __device__ __forceinline__ void load_stage_direct(const RowSet<NLD>& rs, int64_t
 
 // Zero-filling load of a partial stage through VGPRs: chunks at or past
 // kbytes read as zero, so the tail contributes nothing beyond K.
-template <int NLD>
+template <int RSTRIDE, int NLD>
 __device__ __forceinline__ void load_stage_tail(const RowSet<NLD>& rs, int64_t kbyte, int64_t kbytes,
                                                 char* sbase) {
   const int c = threadIdx.x & 7;
@@ -101,7 +102,7 @@ __device__ __forceinline__ void load_stage_tail(const RowSet<NLD>& rs, int64_t k
   for (int p = 0; p < NLD; ++p) {
     i32x4 v = {0, 0, 0, 0};
     if (off < kbytes) v = *reinterpret_cast<const i32x4*>(rs.ptr[p] + off);
-    *reinterpret_cast<i32x4*>(sbase + lds_off(r0 + 32 * p, c)) = v;
+    *reinterpret_cast<i32x4*>(sbase + lds_off(r0 + RSTRIDE * p, c)) = v;
   }
 }
 
@@ -202,23 +203,23 @@ __device__ __forceinline__ void gemm_mainloop(const RowSet<TL::A_LD>& ra, const 
   const int64_t KT = kbytes / TL::ROWB;   // full stages
   if (kbytes % TL::ROWB != 0) {
     char* sb = lds + TL::STAGE_BYTES;
-    load_stage_tail<TL::A_LD>(ra, KT * TL::ROWB, kbytes, sb);
-    load_stage_tail<TL::B_LD>(rb, KT * TL::ROWB, kbytes, sb + TL::BM * TL::ROWB);
+    load_stage_tail<TL::RSTRIDE, TL::A_LD>(ra, KT * TL::ROWB, kbytes, sb);
+    load_stage_tail<TL::RSTRIDE, TL::B_LD>(rb, KT * TL::ROWB, kbytes, sb + TL::BM * TL::ROWB);
     __syncthreads();
     mma_stage<TL>(sb, sb + TL::BM * TL::ROWB, wm, wn, acc);
     __syncthreads();
   }
   if (KT == 0) return;
-  load_stage_direct<TL::A_LD>(ra, 0, lds);
-  load_stage_direct<TL::B_LD>(rb, 0, lds + TL::BM * TL::ROWB);
+  load_stage_direct<TL::NWAVES, TL::A_LD>(ra, 0, lds);
+  load_stage_direct<TL::NWAVES, TL::B_LD>(rb, 0, lds + TL::BM * TL::ROWB);
   wait_vmem();
   __syncthreads();
   for (int64_t kt = 0; kt < KT; ++kt) {
     char* cur = lds + (kt & 1) * TL::STAGE_BYTES;
     char* nxt = lds + ((kt + 1) & 1) * TL::STAGE_BYTES;
     if (kt + 1 < KT) {
-      load_stage_direct<TL::A_LD>(ra, (kt + 1) * TL::ROWB, nxt);
-      load_stage_direct<TL::B_LD>(rb, (kt + 1) * TL::ROWB, nxt + TL::BM * TL::ROWB);
+      load_stage_direct<TL::NWAVES, TL::A_LD>(ra, (kt + 1) * TL::ROWB, nxt);
+      load_stage_direct<TL::NWAVES, TL::B_LD>(rb, (kt + 1) * TL::ROWB, nxt + TL::BM * TL::ROWB);
     }
     mma_stage<TL>(cur, cur + TL::BM * TL::ROWB, wm, wn, acc);
     wait_vmem();

@@ -46,7 +46,7 @@ struct DenseArgs {
 };
 
 template <class TL, int RED, int OUT>
-__global__ __launch_bounds__(256) void fgemm_kernel(DenseArgs a, EpiArgs ep) {
+__global__ __launch_bounds__(TL::THREADS) void fgemm_kernel(DenseArgs a, EpiArgs ep) {
   __shared__ __attribute__((aligned(16))) char lds[DenseLds<TL>::BYTES];
   const int tm = blockIdx.x / a.tiles_n, tn = blockIdx.x % a.tiles_n;
   const int m0 = tm * TL::BM, n0 = tn * TL::BN;
@@ -57,12 +57,12 @@ __global__ __launch_bounds__(256) void fgemm_kernel(DenseArgs a, EpiArgs ep) {
   RowSet<TL::B_LD> rb;
 #pragma unroll
   for (int p = 0; p < TL::A_LD; ++p) {
-    const int m = m0 + r0 + 32 * p;
+    const int m = m0 + r0 + TL::RSTRIDE * p;
     ra.ptr[p] = a.A + (int64_t)(m < a.M ? m : a.M - 1) * rowbytes;
   }
 #pragma unroll
   for (int p = 0; p < TL::B_LD; ++p) {
-    const int n = n0 + r0 + 32 * p;
+    const int n = n0 + r0 + TL::RSTRIDE * p;
     rb.ptr[p] = a.W + (int64_t)(n < a.N ? n : a.N - 1) * rowbytes;
   }
 
@@ -132,25 +132,34 @@ __global__ __launch_bounds__(256) void lse_combine_kernel(const float2* ws, floa
 // kernel table
 
 typedef Tile<In::F32, 64, 128> TileF32;
-typedef Tile<In::BF16, 256, 128> TileBig;
+typedef Tile<In::BF16, 256, 128, 4, 2> TileBig;
 typedef Tile<In::BF16, 128, 128> TileMid;
 
 enum Cfg : int { CFG_F32 = 0, CFG_BF16_256x128 = 1, CFG_BF16_128x128 = 2 };
 
 typedef void (*KernelFn)(DenseArgs, EpiArgs);
 
+struct KernelChoice {
+  KernelFn fn;
+  int threads;
+};
+
 template <class TL>
-static KernelFn pick_kernel(int red, int out) {
+static KernelChoice pick_kernel(int red, int out) {
+  KernelFn fn = nullptr;
   switch (red) {
     case FG_RED_NONE:
-      return out == OUT_BF16 ? fgemm_kernel<TL, FG_RED_NONE, OUT_BF16> : fgemm_kernel<TL, FG_RED_NONE, OUT_F32>;
+      fn = out == OUT_BF16 ? fgemm_kernel<TL, FG_RED_NONE, OUT_BF16> : fgemm_kernel<TL, FG_RED_NONE, OUT_F32>;
+      break;
     case FG_RED_LOGSUMEXP_ROW:
-      return fgemm_kernel<TL, FG_RED_LOGSUMEXP_ROW, OUT_F32>;
+      fn = fgemm_kernel<TL, FG_RED_LOGSUMEXP_ROW, OUT_F32>;
+      break;
     case FG_RED_GROUPNORM:
-      return out == OUT_BF16 ? fgemm_kernel<TL, FG_RED_GROUPNORM, OUT_BF16>
-                             : fgemm_kernel<TL, FG_RED_GROUPNORM, OUT_F32>;
+      fn = out == OUT_BF16 ? fgemm_kernel<TL, FG_RED_GROUPNORM, OUT_BF16>
+                           : fgemm_kernel<TL, FG_RED_GROUPNORM, OUT_F32>;
+      break;
   }
-  return nullptr;
+  return KernelChoice{fn, TL::THREADS};
 }
 
 }  // namespace fg
@@ -317,16 +326,16 @@ extern "C" fg_status fgemm_run(const fg_plan* plan, const void* A, const void* W
     ep.b[i] = p.epi.ops[i].b;
   }
   const int out_k = p.out_dt == FG_BF16 ? OUT_BF16 : OUT_F32;
-  KernelFn fn = nullptr;
+  KernelChoice kc{nullptr, 0};
   switch (p.cfg) {
-    case CFG_F32: fn = pick_kernel<TileF32>(red, out_k); break;
-    case CFG_BF16_256x128: fn = pick_kernel<TileBig>(red, out_k); break;
-    case CFG_BF16_128x128: fn = pick_kernel<TileMid>(red, out_k); break;
+    case CFG_F32: kc = pick_kernel<TileF32>(red, out_k); break;
+    case CFG_BF16_256x128: kc = pick_kernel<TileBig>(red, out_k); break;
+    case CFG_BF16_128x128: kc = pick_kernel<TileMid>(red, out_k); break;
   }
-  if (fn == nullptr) return fail(FG_ERR_UNSUPPORTED, "fgemm_run: no kernel for this plan");
+  if (kc.fn == nullptr) return fail(FG_ERR_UNSUPPORTED, "fgemm_run: no kernel for this plan");
   hipStream_t s = static_cast<hipStream_t>(stream);
   const unsigned grid = (unsigned)(p.tiles_m * p.tiles_n);
-  hipLaunchKernelGGL(fn, dim3(grid), dim3(256), 0, s, a, ep);
+  hipLaunchKernelGGL(kc.fn, dim3(grid), dim3(kc.threads), 0, s, a, ep);
   if (red == FG_RED_LOGSUMEXP_ROW) {
     const unsigned g2 = (unsigned)((p.M + 3) / 4);
     hipLaunchKernelGGL(lse_combine_kernel, dim3(g2), dim3(256), 0, s, a.ws, static_cast<float*>(out),

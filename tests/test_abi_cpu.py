@@ -144,3 +144,39 @@ def test_status_strings():
     for st in range(6):
         assert L.status_str(st).startswith("FG_")
     assert "unknown" in L.status_str(42)
+
+
+def test_moe_workspace_and_validation():
+    d = L.moe_desc(4096, 2880, 2880, 32, 4)
+    ws = L.moe_workspace_bytes(d)
+    S = 4096 * 4
+    assert ws >= S * 2880 * 2 * 2          # h and the per-slot outputs, bf16
+    d8 = L.moe_desc(4096, 2880, 2880, 32, 4, "e4m3")
+    assert L.moe_workspace_bytes(d8) > ws   # plus quantised activations and scales
+    assert L.moe_workspace_bytes(L.moe_desc(8, 100, 64, 8, 2)) == 0   # invalid -> 0
+    fake = 1 << 40
+    cases = [
+        (L.moe_desc(8, 100, 64, 8, 2), L.FG_ERR_ALIGNMENT),            # H % 64
+        (L.moe_desc(8, 128, 64, 0, 1), L.FG_ERR_INVALID_ARG),          # E = 0
+        (L.moe_desc(8, 128, 64, 300, 2), L.FG_ERR_INVALID_ARG),        # E > 256
+        (L.moe_desc(8, 128, 64, 8, 9), L.FG_ERR_INVALID_ARG),          # top_k > 8
+        (L.moe_desc(8, 128, 64, 2, 3), L.FG_ERR_INVALID_ARG),          # top_k > E
+        (L.moe_desc(8, 128, 64, 8, 2, "f32"), L.FG_ERR_UNSUPPORTED),
+        (L.moe_desc(-1, 128, 64, 8, 2), L.FG_ERR_INVALID_ARG),
+        (L.moe_desc(8, 128, 64, 8, 2, limit=-1.0), L.FG_ERR_INVALID_ARG),
+    ]
+    for desc, want in cases:
+        with pytest.raises(L.FgError) as ei:
+            L.moe_grouped_ffn(desc, *([fake] * 12), 1 << 30, None)
+        assert ei.value.status == want, (desc.T, desc.H, desc.E, desc.top_k)
+    d = L.moe_desc(8, 128, 64, 8, 2)
+    with pytest.raises(L.FgError) as ei:                                   # workspace too small
+        L.moe_grouped_ffn(d, *([fake] * 11), None, 0, None)
+    assert ei.value.status == L.FG_ERR_WORKSPACE
+    with pytest.raises(L.FgError) as ei:                                   # e4m3 without scales
+        L.moe_grouped_ffn(L.moe_desc(8, 128, 64, 8, 2, "e4m3"), fake, fake, fake, fake, None, None,
+                          fake, fake, fake, fake, fake, fake, 1 << 30, None)
+    assert ei.value.status == L.FG_ERR_INVALID_ARG
+    with pytest.raises(L.FgError) as ei:                                   # misaligned tokens
+        L.moe_grouped_ffn(d, fake + 4, *([fake] * 11), 1 << 30, None)
+    assert ei.value.status == L.FG_ERR_ALIGNMENT

@@ -269,3 +269,42 @@ def test_synth_moe_shapes_small():
     wf = bf16_decode(w["w_gate_up"])
     assert np.max(np.abs(d - wf)) <= 2.0 ** -4 * np.max(np.abs(wf)) + 1e-3
     assert math.isfinite(float(d.sum()))
+
+
+def test_storage_deviation_bound():
+    """The flip bound is zero away from rounding boundaries and covers the
+    other rounding decision at a boundary (bf16 and bf16→e4m3 storage)."""
+    from oracle.moe import storage_deviation, FRAGILE_REL
+    # exactly representable values: no decision is fragile
+    h = np.array([[1.0, 0.5, -2.0, 0.75]])
+    for st in ("bf16", "e4m3"):
+        stored, dev = storage_deviation(h, st)
+        assert np.all(dev == 0.0)
+    # an element right at a bf16 midpoint: both roundings are legitimate
+    mid = 1.0 + 2.0 ** -8
+    h = np.array([[mid * (1 + 1e-9), 0.3, 0.2]])
+    stored, dev = storage_deviation(h, "bf16")
+    other = 1.0 if stored[0, 0] != 1.0 else 1.0 + 2.0 ** -7
+    assert dev[0, 0] >= abs(other - stored[0, 0]) and dev[0, 2] == 0.0
+    # e4m3 with scale 1 (row max 448): 1.06640625 is the midpoint of the bf16 values
+    # 1.0625 (an e4m3 tie, rounds to 1.0) and 1.0703125 (rounds to 1.125), so the
+    # stored e4m3 value may legitimately be either 1.0 or 1.125
+    h = np.array([[448.0, 1.06640625 * (1 + 1e-9), 3.0]])
+    stored, dev = storage_deviation(h, "e4m3")
+    assert stored[0, 1] == 1.125 and dev[0, 1] == 0.125 and dev[0, 2] == 0.0
+    # a value at an e4m3 tie that bf16 keeps exactly: both sides decide alike
+    h = np.array([[448.0, 1.0625 * (1 - 1e-9), 3.0]])
+    stored, dev = storage_deviation(h, "e4m3")
+    assert stored[0, 1] == 1.0 and dev[0, 1] == 0.0
+    # the MoE bound is zero for storage "none" and non-negative otherwise
+    rng = np.random.default_rng(21)
+    x = rng.standard_normal((6, 8))
+    Wgu = rng.standard_normal((2, 8, 8)) * 0.3
+    Wd = rng.standard_normal((2, 8, 4)) * 0.3
+    r = ref_moe(x, rng.standard_normal((6, 2)), (Wgu, Wd), 2, storage="none", with_bound=True)
+    assert np.all(r["out_bound"] == 0.0)
+    r2 = ref_moe(x, rng.standard_normal((6, 2)), (Wgu, Wd), 2, storage="e4m3", with_bound=True)
+    assert np.all(r2["out_bound"] >= 0.0)
+    r3 = ref_moe(x, rng.standard_normal((6, 2)), (Wgu, Wd), 2, storage="e4m3")
+    assert r3["out"].shape == r2["out"].shape
+    assert FRAGILE_REL < 1e-4
