@@ -31,9 +31,11 @@ constexpr int KMAX = 8;       // largest supported top_k
 constexpr int EMAX = 256;     // largest supported expert count
 
 // ---------------------------------------------------------------------------
-// route: per token, the top-k logits in descending order (ties to the lower
-// expert index: experts are visited in ascending order and a later expert
-// displaces an entry only when strictly larger), then the softmax over them.
+// route: per token, the top-k logits in descending order with ties to the
+// lower expert index, then the softmax over them. The list is kept sorted by
+// the key (value descending, index ascending) with an insertion pass that
+// compares full keys, so an entry displaced downwards still lands ahead of
+// equal values with larger indices.
 
 __global__ __launch_bounds__(256) void moe_route_kernel(const float* logits, int T, int E, int k,
                                                         int32_t* topk_idx, float* topk_w) {
@@ -52,14 +54,15 @@ __global__ __launch_bounds__(256) void moe_route_kernel(const float* logits, int
     int id = e;
 #pragma unroll
     for (int p = 0; p < KMAX; ++p) {
-      if (bi[p] < 0 || v > bv[p]) {
-        const float tv = bv[p];
-        const int ti = bi[p];
-        bv[p] = v;
-        bi[p] = id;
-        v = tv;
-        id = ti;
-      }
+      // branch-free compare-exchange on the key (value desc, index asc); an
+      // empty slot (index −1) always takes the carried entry
+      const bool take = (bi[p] < 0) | (v > bv[p]) | ((v == bv[p]) & (id < bi[p]));
+      const float nv = take ? v : bv[p];
+      const int ni = take ? id : bi[p];
+      v = take ? bv[p] : v;
+      id = take ? bi[p] : id;
+      bv[p] = nv;
+      bi[p] = ni;
     }
   }
   float ex[KMAX], sum = 0.0f;
