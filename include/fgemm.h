@@ -174,7 +174,7 @@ size_t moe_workspace_bytes(const moe_desc *d);
  *   s_down         [E, H] fp32 per-row weight scales (e4m3 only, else NULL).
  *   out            [T, H] bf16: out[t] = Σ_j w[t,j]·FFN_{idx[t,j]}(tokens[t]).
  *   topk_idx       [T, top_k] int32 out: selected experts, logits descending,
- *                  ties to the lower expert index.
+ *                  ties to the lower expert index (a NaN logit ranks as −∞).
  *   topk_w         [T, top_k] fp32 out: softmax over the selected logits.
  *   perm           [T·top_k] int32 out: slot ids p = t·top_k + j sorted by
  *                  (expert, p) — stable, hence unique.

@@ -26,8 +26,9 @@ The oracle takes the block's steps in order, each as its plain definition:
             h is stored in the method's declared intermediate format,
             modelled here: bf16 RNE; in the W8A8 variant the bf16 h is
             then quantised per row to e4m3 with an fp32 scale;
-            y_slot[rows] = h·W_d[e]ᵀ
-  finalize  out[t] = Σ_j w[t, j]·y_slot[t·k + j], j ascending
+            y_slot[rows] = h·W_d[e]ᵀ, multiplied by the routing weight of
+            each slot and stored as bf16 (RNE), the method's declared format
+  finalize  out[t] = Σ_j y_slot[t·k + j], j ascending
 
 fp8 (W8A8) variant: weights are stored as e4m3 codes with one fp32 scale per
 output row (decoded before they reach this oracle); activations (x per
@@ -174,7 +175,7 @@ def ref_expert_rows(X, W_gu, W_d, storage="bf16", act_quant=False, alpha=1.702,
 
 
 def ref_moe(x, logits, weights, k, storage="bf16", act_quant=False, alpha=1.702,
-            limit=7.0, interleaved=False, tokens=None, with_bound=False):
+            limit=7.0, interleaved=False, tokens=None, with_bound=False, slot_storage="bf16"):
     """The MoE expert FFN step, fp64.
 
     x: [T, H] fp64 (decoded bf16 tokens); logits: [T, E] (fp32 values);
@@ -182,6 +183,8 @@ def ref_moe(x, logits, weights, k, storage="bf16", act_quant=False, alpha=1.702,
     applied), or a pair of arrays [E, 2I, H], [E, H, I].
     tokens: optional subset of token ids whose outputs to compute (a token's
     output depends only on its own row and its own routing).
+    slot_storage: "bf16" (the routing-weighted slot outputs are stored as
+    bf16 before the finalize sum, as the method declares) or "none".
     with_bound: also return "out_bound", per output element the largest
     change any storage-rounding decision of h within the fragile
     neighbourhood of a boundary (see storage_deviation) can cause; a kernel
@@ -219,13 +222,25 @@ def ref_moe(x, logits, weights, k, storage="bf16", act_quant=False, alpha=1.702,
             y = ref_expert_rows(x[slots // k], W_gu, W_d, storage, act_quant, alpha,
                                 limit, interleaved)
         y_slot[dst] = y
-    # finalize: routing-weighted sum over the k slots of each token, j ascending
+    # the routing weight is applied per slot and the weighted slot output is
+    # stored as bf16; finalize sums the k stored slots of each token, j ascending
     out = np.zeros((tok.size, H), dtype=np.float64)
     bound = np.zeros((tok.size, H), dtype=np.float64) if with_bound else None
     for j in range(k):
-        out += w[tok, j][:, None] * y_slot[j::k]
-        if with_bound:
+        ys = w[tok, j][:, None] * y_slot[j::k]
+        if slot_storage == "bf16":
+            stored = bf16_decode(bf16_encode_rne(ys))
+            if with_bound:
+                # either neighbouring bf16 value is a legitimate rounding of ys
+                # when ys moves within its own bound plus fp32 evaluation noise
+                yb = w[tok, j][:, None] * b_slot[j::k] + FRAGILE_REL * np.abs(ys)
+                lo = bf16_decode(bf16_encode_rne(ys - yb))
+                hi = bf16_decode(bf16_encode_rne(ys + yb))
+                bound += np.maximum(np.abs(lo - stored), np.abs(hi - stored))
+            ys = stored
+        elif with_bound:
             bound += w[tok, j][:, None] * b_slot[j::k]
+        out += ys
     res = {"out": out, "idx": idx, "w": w, "counts": counts, "offsets": offsets, "perm": perm}
     if with_bound:
         res["out_bound"] = bound

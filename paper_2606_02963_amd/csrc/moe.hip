@@ -3,8 +3,9 @@
 // Launch sequence on the caller's stream, with no host synchronisation (the
 // per-expert counts never leave the device):
 //   [e4m3 only] quantise tokens per row          quantize_rows_kernel
-//   route: top-k + softmax per token             moe_route_kernel
-//   histogram, offsets, stable permutation       moe_permute_kernel (one workgroup)
+//   route: top-k + softmax per token, and the    moe_route_kernel
+//     expert histogram of each block of tokens
+//   offsets, stable permutation, m-tile prefix   moe_place_kernel
 //   grouped gate/up GEMM + clamped SwiGLU        grouped_kernel<.., EPI_GATEUP>
 //   [e4m3 only] quantise h per row               quantize_rows_kernel
 //   grouped down GEMM × routing weight           grouped_kernel<.., EPI_DOWN>
@@ -31,120 +32,228 @@ constexpr int KMAX = 8;       // largest supported top_k
 constexpr int EMAX = 256;     // largest supported expert count
 
 // ---------------------------------------------------------------------------
-// route: per token, the top-k logits in descending order with ties to the
-// lower expert index, then the softmax over them. The list is kept sorted by
-// the key (value descending, index ascending) with an insertion pass that
-// compares full keys, so an entry displaced downwards still lands ahead of
-// equal values with larger indices.
+// route: a workgroup covers ROUTE_TOKENS tokens. Their logits are first
+// staged in LDS with one coalesced pass; then one thread per token keeps the
+// top-k in a list sorted by the key (value descending, index ascending), so
+// ties go to the lower expert index, and takes the softmax over the k
+// selected logits. The workgroup also forms the expert histogram of its
+// slots (LDS atomics: integer counts do not depend on the order of the adds).
+//
+// place: the stable permutation. The slots of a workgroup's tokens are
+// split into contiguous per-wave ranges; a slot's position is
+//   offsets[e] + Σ_{b' < b} count[b'][e] + Σ_{w' < w} count_w'[e]
+//   + (earlier slots of expert e in the wave's own range),
+// i.e. its rank in the sort by (expert, slot id). Inside a wave, 64-slot
+// chunks are processed in order and each distinct expert of a chunk takes
+// one ballot. No atomics decide a position, so the result is unique and
+// bit-reproducible. Workgroup 0 also writes offsets and the m-tile prefix
+// the grouped GEMMs read. When one workgroup covers every token, route and
+// place run in the same launch.
 
-__global__ __launch_bounds__(256) void moe_route_kernel(const float* logits, int T, int E, int k,
-                                                        int32_t* topk_idx, float* topk_w) {
-  const int t = blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= T) return;
-  float bv[KMAX];
-  int bi[KMAX];
+constexpr int ROUTE_TOKENS = 64;          // tokens per route / place workgroup
+constexpr int ROUTE_WAVES = 4;
+constexpr int PLACE_WAVES = 4;
+
+__device__ __forceinline__ bool key_wins(float v, int i, float bv, int bi) {
+  return (v > bv) | ((v == bv) & (i < bi));
+}
+
+// Stable placement of the slots [s_begin, s_begin + n_slots) by NW waves.
+// off[e]: the global position of this workgroup's first slot of expert e.
+// wrun: NW × EMAX ints of LDS. Ends after writing perm.
+template <int NW>
+__device__ __forceinline__ void place_slots(const int32_t* topk_idx, int s_begin, int n_slots, int E,
+                                            const int* off, int (*wrun)[EMAX], int32_t* perm) {
+  constexpr int CH = (KMAX * ROUTE_TOKENS / NW + 63) / 64;     // 64-slot chunks per wave, at most
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int e = threadIdx.x; e < E; e += 64 * NW)
 #pragma unroll
-  for (int p = 0; p < KMAX; ++p) {
-    bv[p] = -INFINITY;
-    bi[p] = -1;
-  }
-  const float* row = logits + (int64_t)t * E;
-  for (int e = 0; e < E; ++e) {
-    float v = row[e];
-    int id = e;
+    for (int w = 0; w < NW; ++w) wrun[w][e] = 0;
+  __syncthreads();
+  const int per_wave = (n_slots + NW - 1) / NW;
+  const int s0 = s_begin + wave * per_wave;
+  const int s_end = s_begin + n_slots;
+  const unsigned long long lt = (1ull << lane) - 1ull;
+  int my_e[CH], my_rank[CH];
 #pragma unroll
-    for (int p = 0; p < KMAX; ++p) {
-      // branch-free compare-exchange on the key (value desc, index asc); an
-      // empty slot (index −1) always takes the carried entry
-      const bool take = (bi[p] < 0) | (v > bv[p]) | ((v == bv[p]) & (id < bi[p]));
-      const float nv = take ? v : bv[p];
-      const int ni = take ? id : bi[p];
-      v = take ? bv[p] : v;
-      id = take ? bi[p] : id;
-      bv[p] = nv;
-      bi[p] = ni;
+  for (int c = 0; c < CH; ++c) {
+    my_e[c] = -1;
+    my_rank[c] = 0;
+    if (c * 64 >= per_wave) continue;        // uniform
+    const int s = s0 + c * 64 + lane;
+    const bool valid = (c * 64 + lane < per_wave) && s < s_end;
+    const int e = valid ? topk_idx[s] : -1;
+    my_e[c] = e;
+    unsigned long long pending = __ballot(valid);
+    while (pending) {
+      const int leader = __ffsll((long long)pending) - 1;
+      const int le = __shfl(e, leader, 64);
+      const unsigned long long m = __ballot(valid && e == le);
+      const int run = wrun[wave][le];
+      if (valid && e == le) my_rank[c] = run + __popcll(m & lt);
+      if (lane == leader) wrun[wave][le] = run + __popcll(m);
+      pending &= ~m;
     }
   }
-  float ex[KMAX], sum = 0.0f;
+  __syncthreads();
 #pragma unroll
-  for (int p = 0; p < KMAX; ++p) {
-    ex[p] = p < k ? expf(bv[p] - bv[0]) : 0.0f;
-    sum += ex[p];
-  }
-#pragma unroll
-  for (int p = 0; p < KMAX; ++p) {
-    if (p < k) {
-      topk_idx[(int64_t)t * k + p] = bi[p];
-      topk_w[(int64_t)t * k + p] = ex[p] / sum;
-    }
+  for (int c = 0; c < CH; ++c) {
+    const int e = my_e[c];
+    if (e < 0) continue;
+    int r = off[e] + my_rank[c];
+    for (int w = 0; w < wave; ++w) r += wrun[w][e];
+    perm[r] = s0 + c * 64 + lane;
   }
 }
 
-// ---------------------------------------------------------------------------
-// permute: one workgroup of 16 waves. Wave w owns experts w, w + 16, ...; it
-// walks the S = T·k slot ids in 64-slot chunks and, with one ballot per
-// chunk, counts (pass 1) and then places (pass 2) the slots of its expert:
-// a slot's position is the expert's offset plus the number of its expert's
-// slots with a smaller id. That is the stable sort by (expert, slot id),
-// computed without atomics, so it is unique and bit-reproducible.
-
-constexpr int PERM_THREADS = 1024;
-constexpr int PERM_LDS_SLOTS = 65536;
-
-template <bool IDS_IN_LDS>
-__global__ __launch_bounds__(PERM_THREADS) void moe_permute_kernel(const int32_t* topk_idx, int S, int E, int BM,
-                                                                   int32_t* offsets, int32_t* tile_off,
-                                                                   int32_t* perm) {
-  __shared__ int cnt[EMAX];
-  __shared__ int off[EMAX + 1];
-  __shared__ uint8_t ids_lds[IDS_IN_LDS ? PERM_LDS_SLOTS : 1];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  if constexpr (IDS_IN_LDS) {
-    for (int i = tid; i < S; i += PERM_THREADS) ids_lds[i] = (uint8_t)topk_idx[i];
-    __syncthreads();
-  }
-  auto expert_of = [&](int s) -> int {
-    if constexpr (IDS_IN_LDS) return ids_lds[s];
-    else return topk_idx[s];
-  };
-  for (int e = wave; e < E; e += PERM_THREADS / 64) {
-    int c = 0;
-    for (int base = 0; base < S; base += 64) {
-      const int s = base + lane;
-      const bool m = s < S && expert_of(s) == e;
-      c += __popcll(__ballot(m));
-    }
-    if (lane == 0) cnt[e] = c;
-  }
-  __syncthreads();
-  if (tid == 0) {
+// Exclusive prefix of the per-expert totals `tot` (in place) by one thread;
+// workgroup 0 also publishes offsets and the m-tile prefix.
+__device__ __forceinline__ void publish_offsets(int* tot, int E, int BM, int32_t* offsets, int32_t* tile_off) {
+  if (threadIdx.x == 0) {
     int acc = 0, tacc = 0;
     for (int e = 0; e < E; ++e) {
-      off[e] = acc;
-      offsets[e] = acc;
-      tile_off[e] = tacc;
-      acc += cnt[e];
-      tacc += (cnt[e] + BM - 1) / BM;
+      const int c = tot[e];
+      tot[e] = acc;
+      if (blockIdx.x == 0) {
+        offsets[e] = acc;
+        tile_off[e] = tacc;
+      }
+      acc += c;
+      tacc += (c + BM - 1) / BM;
     }
-    off[E] = acc;
-    offsets[E] = acc;
-    tile_off[E] = tacc;
+    if (blockIdx.x == 0) {
+      offsets[E] = acc;
+      tile_off[E] = tacc;
+    }
   }
   __syncthreads();
-  for (int e = wave; e < E; e += PERM_THREADS / 64) {
-    int run = off[e];
-    for (int base = 0; base < S; base += 64) {
-      const int s = base + lane;
-      const bool m = s < S && expert_of(s) == e;
-      const unsigned long long mask = __ballot(m);
-      if (m) {
-        const int below = __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
-                                                    __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0));
-        perm[run + below] = s;
-      }
-      run += __popcll(mask);
+}
+
+template <bool FUSED_PLACE>
+__global__ __launch_bounds__(64 * ROUTE_WAVES) void moe_route_kernel(const float* logits, int T, int E, int k,
+                                                                     int32_t* topk_idx, float* topk_w,
+                                                                     int32_t* block_counts, int BM,
+                                                                     int32_t* offsets, int32_t* tile_off,
+                                                                     int32_t* perm) {
+  // row pitch E + 1 floats: thread t reading its row's logit e hits bank (t·(E+1) + e) mod 64
+  __shared__ float lg[ROUTE_TOKENS * (EMAX + 1)];
+  __shared__ int hist[EMAX];
+  __shared__ int wrun[FUSED_PLACE ? ROUTE_WAVES : 1][EMAX];
+  const int t0 = blockIdx.x * ROUTE_TOKENS;
+  const int nt = T - t0 < ROUTE_TOKENS ? T - t0 : ROUTE_TOKENS;
+  const int pitch = E + 1;
+  for (int e = threadIdx.x; e < E; e += 64 * ROUTE_WAVES) hist[e] = 0;
+  const float* src = logits + (int64_t)t0 * E;
+  const int n = nt * E;
+  constexpr int UNR = 8;                     // loads in flight per thread before the LDS stores
+  for (int i0 = threadIdx.x; i0 < n; i0 += 64 * ROUTE_WAVES * UNR) {
+    float x[UNR];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int i = i0 + u * 64 * ROUTE_WAVES;
+      x[u] = i < n ? src[i] : 0.0f;
+    }
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int i = i0 + u * 64 * ROUTE_WAVES;
+      if (i < n) lg[(i / E) * pitch + i % E] = x[u];
     }
   }
+  __syncthreads();
+  const int tt = threadIdx.x;
+  if (tt < nt) {
+    // insertion into a list sorted by (value descending, index ascending);
+    // experts arrive in ascending order, an entry is displaced only by a
+    // larger key, and the compare-exchange is branch-free
+    float bv[KMAX];
+    int bi[KMAX];
+#pragma unroll
+    for (int p = 0; p < KMAX; ++p) {
+      bv[p] = -INFINITY;
+      bi[p] = -1;
+    }
+    const float* row = lg + tt * pitch;
+    for (int e = 0; e < E; ++e) {
+      const float x = row[e];
+      float v = x != x ? -INFINITY : x;     // a NaN logit ranks as −∞, so k experts are always selected
+      int id = e;
+#pragma unroll
+      for (int p = 0; p < KMAX; ++p) {
+        const bool take = (bi[p] < 0) | key_wins(v, id, bv[p], bi[p]);
+        const float nv = take ? v : bv[p];
+        const int ni = take ? id : bi[p];
+        v = take ? bv[p] : v;
+        id = take ? bi[p] : id;
+        bv[p] = nv;
+        bi[p] = ni;
+      }
+    }
+    float ex[KMAX], sum = 0.0f;
+#pragma unroll
+    for (int p = 0; p < KMAX; ++p) {
+      ex[p] = p < k ? expf(bv[p] - bv[0]) : 0.0f;
+      sum += ex[p];
+    }
+    const int t = t0 + tt;
+#pragma unroll
+    for (int p = 0; p < KMAX; ++p) {
+      if (p < k) {
+        topk_idx[(int64_t)t * k + p] = bi[p];
+        topk_w[(int64_t)t * k + p] = ex[p] / sum;
+        atomicAdd(&hist[bi[p]], 1);
+      }
+    }
+  }
+  __syncthreads();
+  if constexpr (FUSED_PLACE) {
+    // the only workgroup: its histogram is the total; topk_idx written above
+    // by this workgroup is visible after the barrier
+    publish_offsets(hist, E, BM, offsets, tile_off);
+    place_slots<ROUTE_WAVES>(topk_idx, 0, T * k, E, hist, wrun, perm);
+  } else {
+    for (int e = threadIdx.x; e < E; e += 64 * ROUTE_WAVES) block_counts[(int64_t)blockIdx.x * E + e] = hist[e];
+  }
+}
+
+__global__ __launch_bounds__(64 * PLACE_WAVES) void moe_place_kernel(const int32_t* topk_idx, const int32_t* block_counts,
+                                                                     int S, int E, int k, int nblocks, int BM,
+                                                                     int32_t* offsets, int32_t* tile_off,
+                                                                     int32_t* perm) {
+  __shared__ int tot[EMAX];
+  __shared__ int before[EMAX];
+  __shared__ int wrun[PLACE_WAVES][EMAX];
+  for (int e = threadIdx.x; e < E; e += 64 * PLACE_WAVES) {
+    tot[e] = 0;
+    before[e] = 0;
+  }
+  __syncthreads();
+  // per-expert totals and the counts of earlier workgroups, summed by all
+  // threads in parallel (integer LDS atomics: order-independent)
+  const int n = nblocks * E;
+  constexpr int UNR = 8;                     // loads in flight per thread before the LDS adds
+  for (int i0 = threadIdx.x; i0 < n; i0 += 64 * PLACE_WAVES * UNR) {
+    int c[UNR];
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int i = i0 + u * 64 * PLACE_WAVES;
+      c[u] = i < n ? block_counts[i] : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < UNR; ++u) {
+      const int i = i0 + u * 64 * PLACE_WAVES;
+      if (i < n) {
+        atomicAdd(&tot[i % E], c[u]);
+        if (i / E < (int)blockIdx.x) atomicAdd(&before[i % E], c[u]);
+      }
+    }
+  }
+  __syncthreads();
+  publish_offsets(tot, E, BM, offsets, tile_off);
+  for (int e = threadIdx.x; e < E; e += 64 * PLACE_WAVES) before[e] += tot[e];
+  __syncthreads();
+  const int s_begin = blockIdx.x * ROUTE_TOKENS * k;
+  const int n_slots = (S - s_begin) < ROUTE_TOKENS * k ? S - s_begin : ROUTE_TOKENS * k;
+  place_slots<PLACE_WAVES>(topk_idx, s_begin, n_slots, E, before, wrun, perm);
 }
 
 // ---------------------------------------------------------------------------
@@ -165,7 +274,9 @@ struct GroupedArgs {
   const int32_t* tile_off; // [E + 1]
   const float* topk_w;     // [S] routing weights by slot id
   char* out;               // gate/up: h [S, I] bf16 (expert order); down: y_slot [S, H] bf16 (slot order)
-  int E, k, tiles_n;
+  int E, k;
+  int tiles_n;             // n-tiles of the output
+  int tiles_n_grid;        // n-tiles per grid row: tiles_n rounded up to a multiple of 8
   int64_t K;               // contraction length in elements
   int64_t Nw;              // weight rows per expert: 2I or H
   int64_t I;               // intermediate size (gate/up pairing)
@@ -200,9 +311,12 @@ __device__ __forceinline__ int64_t weight_row(const GroupedArgs& a, int tn, int 
 template <class TL, int EPI>
 __global__ __launch_bounds__(TL::THREADS) void grouped_kernel(GroupedArgs a) {
   __shared__ __attribute__((aligned(16))) char lds[GroupedLds<TL>::BYTES];
-  const int tn = blockIdx.x % a.tiles_n;
-  const int mt = blockIdx.x / a.tiles_n;
-  if (mt >= a.tile_off[a.E]) return;
+  // n fastest; with tiles_n_grid a multiple of 8 and workgroups dealt to the
+  // 8 XCDs round-robin, every m-tile of a given n-tile runs on the same XCD,
+  // so the weight tile is fetched into one L2 and reused there
+  const int tn = blockIdx.x % a.tiles_n_grid;
+  const int mt = blockIdx.x / a.tiles_n_grid;
+  if (tn >= a.tiles_n || mt >= a.tile_off[a.E]) return;
   int lo = 0, hi = a.E;        // tile_off[lo] ≤ mt < tile_off[hi]
   while (hi - lo > 1) {
     const int mid = (lo + hi) >> 1;
@@ -336,6 +450,9 @@ __global__ __launch_bounds__(256) void fill_i32_kernel(int32_t* p, int n, int v)
 // ---------------------------------------------------------------------------
 // host side
 
+// Prefill tiles are 128 × 128 (4 waves): on the T = 4096 step they measured
+// faster than 192- and 256-row tiles, whose ragged last m-tile per expert
+// (n_e ≈ 512 ± 22 slots) wastes more of the matrix cores.
 typedef Tile<In::BF16, 128, 128> GBf16Big;
 typedef Tile<In::BF16, 32, 128> GBf16Small;
 typedef Tile<In::E4M3, 128, 128> GF8Big;
@@ -344,22 +461,31 @@ typedef Tile<In::E4M3, 32, 128> GF8Small;
 struct MoeLayout {
   int64_t S;
   int BM;
-  size_t tile_off, h, y, xq, sx, hq, sh, total;
+  int nblocks;             // route / place workgroups
+  size_t tile_off, counts, h, y, xq, sx, hq, sh, total;
 };
 
 static size_t align_up(size_t v) { return (v + 255) & ~(size_t)255; }
 
-// Row tile of the grouped GEMMs: 128 rows when experts average more than 48
-// slots, else 32 (decode: a handful of rows per expert, weight streaming).
-static int pick_bm(int64_t S, int E) { return S > (int64_t)48 * E ? 128 : 32; }
+// Row tile of the grouped GEMMs: the big tile when experts average more than
+// 48 slots, else the 32-row tile (decode: a handful of rows per expert, weight
+// streaming). The launch dispatches on the same predicate, and the m-tile
+// prefix is built with the chosen tile's BM.
+static bool use_big_tiles(int64_t S, int E) { return S > (int64_t)48 * E; }
+static int pick_bm(int64_t S, int E) { return use_big_tiles(S, E) ? GBf16Big::BM : GBf16Small::BM; }
+static_assert(GBf16Big::BM == GF8Big::BM && GBf16Small::BM == GF8Small::BM,
+              "bf16 and e4m3 tiles must share BM: one m-tile prefix serves both");
 
 static MoeLayout layout(const moe_desc& d) {
   MoeLayout L;
   L.S = d.T * d.top_k;
   L.BM = pick_bm(L.S, d.E);
   size_t o = 0;
+  L.nblocks = (int)((d.T + ROUTE_TOKENS - 1) / ROUTE_TOKENS);
   L.tile_off = o;
   o = align_up(o + sizeof(int32_t) * (size_t)(d.E + 1));
+  L.counts = o;
+  o = align_up(o + sizeof(int32_t) * (size_t)L.nblocks * (size_t)d.E);
   L.h = o;
   o = align_up(o + (size_t)L.S * (size_t)d.I * 2);
   L.y = o;
@@ -400,10 +526,14 @@ static fg_status validate_desc(const moe_desc* d, const char* fn) {
   return FG_OK;
 }
 
+// n-tiles: gate/up tiles cover BN/2 columns of h (BN weight rows, gate and
+// up interleaved), down tiles BN columns of the output.
 template <class TL, int EPI>
-static void launch_grouped(const GroupedArgs& a, int64_t S, hipStream_t s) {
+static void launch_grouped(GroupedArgs a, int64_t S, hipStream_t s) {
+  a.tiles_n = EPI == EPI_GATEUP ? (int)(a.I / (TL::BN / 2)) : (int)((a.Nw + TL::BN - 1) / TL::BN);
+  a.tiles_n_grid = (a.tiles_n + 7) / 8 * 8;
   const int64_t mtiles = (S + (int64_t)a.E * (TL::BM - 1)) / TL::BM;
-  const unsigned grid = (unsigned)(mtiles * a.tiles_n);
+  const unsigned grid = (unsigned)(mtiles * a.tiles_n_grid);
   hipLaunchKernelGGL((grouped_kernel<TL, EPI>), dim3(grid), dim3(TL::THREADS), 0, s, a);
 }
 
@@ -460,14 +590,17 @@ extern "C" fg_status moe_grouped_ffn(const moe_desc* d, const void* tokens, cons
                        static_cast<const uint16_t*>(tokens), d->T, d->H, reinterpret_cast<uint8_t*>(ws + L.xq), sx);
     a_tokens = ws + L.xq;
   }
-  hipLaunchKernelGGL(moe_route_kernel, dim3((unsigned)((T + 255) / 256)), dim3(256), 0, s, router_logits, T, d->E,
-                     d->top_k, topk_idx, topk_w);
-  if (S <= PERM_LDS_SLOTS)
-    hipLaunchKernelGGL(moe_permute_kernel<true>, dim3(1), dim3(PERM_THREADS), 0, s, topk_idx, (int)S, d->E, L.BM,
-                       expert_offsets, tile_off, perm);
-  else
-    hipLaunchKernelGGL(moe_permute_kernel<false>, dim3(1), dim3(PERM_THREADS), 0, s, topk_idx, (int)S, d->E,
-                       L.BM, expert_offsets, tile_off, perm);
+  int32_t* counts = reinterpret_cast<int32_t*>(ws + L.counts);
+  if (L.nblocks == 1) {
+    hipLaunchKernelGGL(moe_route_kernel<true>, dim3(1), dim3(64 * ROUTE_WAVES), 0, s, router_logits, T, d->E,
+                       d->top_k, topk_idx, topk_w, counts, L.BM, expert_offsets, tile_off, perm);
+  } else {
+    hipLaunchKernelGGL(moe_route_kernel<false>, dim3((unsigned)L.nblocks), dim3(64 * ROUTE_WAVES), 0, s,
+                       router_logits, T, d->E, d->top_k, topk_idx, topk_w, counts, L.BM, expert_offsets, tile_off,
+                       perm);
+    hipLaunchKernelGGL(moe_place_kernel, dim3((unsigned)L.nblocks), dim3(64 * PLACE_WAVES), 0, s, topk_idx, counts,
+                       (int)S, d->E, d->top_k, L.nblocks, L.BM, expert_offsets, tile_off, perm);
+  }
 
   GroupedArgs g;
   g.perm = perm;
@@ -490,12 +623,11 @@ extern "C" fg_status moe_grouped_ffn(const moe_desc* d, const void* tokens, cons
   g.K = d->H;
   g.Nw = 2 * d->I;
   g.ldo = d->I;
-  g.tiles_n = (int)(d->I / 64);
   if (f8) {
-    if (L.BM == 128) launch_grouped<GF8Big, EPI_GATEUP>(g, S, s);
+    if (use_big_tiles(S, d->E)) launch_grouped<GF8Big, EPI_GATEUP>(g, S, s);
     else launch_grouped<GF8Small, EPI_GATEUP>(g, S, s);
   } else {
-    if (L.BM == 128) launch_grouped<GBf16Big, EPI_GATEUP>(g, S, s);
+    if (use_big_tiles(S, d->E)) launch_grouped<GBf16Big, EPI_GATEUP>(g, S, s);
     else launch_grouped<GBf16Small, EPI_GATEUP>(g, S, s);
   }
 
@@ -516,12 +648,11 @@ extern "C" fg_status moe_grouped_ffn(const moe_desc* d, const void* tokens, cons
   g.K = d->I;
   g.Nw = d->H;
   g.ldo = d->H;
-  g.tiles_n = (int)((d->H + 127) / 128);
   if (f8) {
-    if (L.BM == 128) launch_grouped<GF8Big, EPI_DOWN>(g, S, s);
+    if (use_big_tiles(S, d->E)) launch_grouped<GF8Big, EPI_DOWN>(g, S, s);
     else launch_grouped<GF8Small, EPI_DOWN>(g, S, s);
   } else {
-    if (L.BM == 128) launch_grouped<GBf16Big, EPI_DOWN>(g, S, s);
+    if (use_big_tiles(S, d->E)) launch_grouped<GBf16Big, EPI_DOWN>(g, S, s);
     else launch_grouped<GBf16Small, EPI_DOWN>(g, S, s);
   }
 

@@ -73,6 +73,7 @@ SMALL = [
     MoeSpec("many_experts", T=300, H=128, I=64, E=64, k=8),               # empty experts likely
     MoeSpec("clamps_hit", T=64, H=128, I=128, E=4, k=2, x_std=10.0, w_std=0.05),
     MoeSpec("dense_E1", T=100, H=128, I=64, E=1, k=1),
+    MoeSpec("prefill_big", T=2048, H=512, I=256, E=8, k=4),             # cancellation across slots
 ]
 
 

@@ -128,7 +128,9 @@ def _mp_bruteforce_moe(x, lg, Wgu, Wd, k, alpha=1.702, limit=7.0):
                 h.append(mp.mpf(float(bf16_decode(bf16_encode_rne(np.array([float(hv)])))[0])))
             for n in range(H):
                 y = mp.fsum(h[i] * mp.mpf(float(Wd[e, n, i])) for i in range(I))
-                acc[n] += ex[j] / den * y
+                # the routing-weighted slot output is stored as bf16 before the sum
+                ys = float(bf16_decode(bf16_encode_rne(np.array([float(ex[j] / den * y)])))[0])
+                acc[n] += mp.mpf(ys)
         out[t] = [float(v) for v in acc]
     return out
 
@@ -155,7 +157,8 @@ def test_moe_single_expert_is_dense_ffn():
     x = rng.standard_normal((T, H))
     Wgu = rng.standard_normal((1, 2 * I, H)) * 0.5
     Wd = rng.standard_normal((1, H, I)) * 0.5
-    got = ref_moe(x, rng.standard_normal((T, 1)), (Wgu, Wd), 1, storage="none")["out"]
+    got = ref_moe(x, rng.standard_normal((T, 1)), (Wgu, Wd), 1, storage="none",
+                  slot_storage="none")["out"]
     G = ref_fgemm(x, Wgu[0])
     h = ref_swiglu_clamped(G[:, :I], G[:, I:])
     np.testing.assert_allclose(got, ref_fgemm(h, Wd[0]), rtol=1e-14, atol=1e-14)
@@ -170,7 +173,7 @@ def test_moe_identical_experts_and_zero_down():
     Wgu = np.stack([wgu1] * E)
     Wd = np.stack([wd1] * E)
     lg = rng.standard_normal((T, E))
-    got = ref_moe(x, lg, (Wgu, Wd), 3, storage="none")["out"]
+    got = ref_moe(x, lg, (Wgu, Wd), 3, storage="none", slot_storage="none")["out"]
     G = x @ wgu1.T
     want = ref_swiglu_clamped(G[:, :I], G[:, I:]) @ wd1.T
     np.testing.assert_allclose(got, want, rtol=1e-13, atol=1e-13)
@@ -185,10 +188,10 @@ def test_interleaved_gate_up_is_a_row_permutation():
     Wgu = rng.standard_normal((1, 2 * I, H))
     Wd = rng.standard_normal((1, H, I))
     lg = np.zeros((T, 1))
-    a = ref_moe(x, lg, (Wgu, Wd), 1, storage="none")["out"]
+    a = ref_moe(x, lg, (Wgu, Wd), 1, storage="none", slot_storage="none")["out"]
     inter = np.empty_like(Wgu)
     inter[0, 0::2], inter[0, 1::2] = Wgu[0, :I], Wgu[0, I:]
-    b = ref_moe(x, lg, (inter, Wd), 1, storage="none", interleaved=True)["out"]
+    b = ref_moe(x, lg, (inter, Wd), 1, storage="none", interleaved=True, slot_storage="none")["out"]
     np.testing.assert_allclose(a, b, rtol=1e-15, atol=1e-15)
 
 
@@ -301,7 +304,8 @@ def test_storage_deviation_bound():
     x = rng.standard_normal((6, 8))
     Wgu = rng.standard_normal((2, 8, 8)) * 0.3
     Wd = rng.standard_normal((2, 8, 4)) * 0.3
-    r = ref_moe(x, rng.standard_normal((6, 2)), (Wgu, Wd), 2, storage="none", with_bound=True)
+    r = ref_moe(x, rng.standard_normal((6, 2)), (Wgu, Wd), 2, storage="none", with_bound=True,
+                slot_storage="none")
     assert np.all(r["out_bound"] == 0.0)
     r2 = ref_moe(x, rng.standard_normal((6, 2)), (Wgu, Wd), 2, storage="e4m3", with_bound=True)
     assert np.all(r2["out_bound"] >= 0.0)
