@@ -33,97 +33,120 @@ constexpr int EMAX = 256;     // largest supported expert count
 
 // ---------------------------------------------------------------------------
 // route: a workgroup covers ROUTE_TOKENS tokens. Their logits are first
-// staged in LDS with one coalesced pass; then one thread per token keeps the
-// top-k in a list sorted by the key (value descending, index ascending), so
-// ties go to the lower expert index, and takes the softmax over the k
-// selected logits. The workgroup also forms the expert histogram of its
-// slots (LDS atomics: integer counts do not depend on the order of the adds).
+// staged in LDS with one coalesced pass; then four lanes per token select the
+// top-k by descending key (value descending, ties to the lower expert index)
+// and take the softmax over the k selected logits. The workgroup also forms
+// the expert histogram of its slots (LDS atomics: integer counts do not
+// depend on the order of the adds).
 //
-// place: the stable permutation. The slots of a workgroup's tokens are
-// split into contiguous per-wave ranges; a slot's position is
-//   offsets[e] + Σ_{b' < b} count[b'][e] + Σ_{w' < w} count_w'[e]
-//   + (earlier slots of expert e in the wave's own range),
-// i.e. its rank in the sort by (expert, slot id). Inside a wave, 64-slot
-// chunks are processed in order and each distinct expert of a chunk takes
-// one ballot. No atomics decide a position, so the result is unique and
-// bit-reproducible. Workgroup 0 also writes offsets and the m-tile prefix
-// the grouped GEMMs read. When one workgroup covers every token, route and
-// place run in the same launch.
+// place: the stable permutation. A slot's position is
+//   offsets[e] + Σ_{b' < b} count[b'][e] + (earlier slots of expert e in
+//   its own workgroup's range),
+// i.e. its rank in the sort by (expert, slot id); the last term comes from
+// per-expert slot bitmasks. No atomic decides a position, so the result is
+// unique and bit-reproducible. Workgroup 0 also writes offsets and the
+// m-tile prefix the grouped GEMMs read. When one workgroup covers every
+// token, route and place run in the same launch.
 
 constexpr int ROUTE_TOKENS = 64;          // tokens per route / place workgroup
-constexpr int ROUTE_WAVES = 4;
+constexpr int ROUTE_WAVES = 4;            // four lanes per token
+static_assert(ROUTE_WAVES * 64 == 4 * ROUTE_TOKENS, "route workgroups hold four lanes per token");
 constexpr int PLACE_WAVES = 4;
 
-__device__ __forceinline__ bool key_wins(float v, int i, float bv, int bi) {
-  return (v > bv) | ((v == bv) & (i < bi));
+// Sortable 64-bit key of (logit, expert). The float's bits are mapped so that
+// unsigned order is numeric order (negative values: all bits flipped;
+// non-negative: sign bit set). −0 is first made +0 so that the two zeros,
+// which compare equal, tie-break by index like any equal pair. A NaN logit
+// ranks as −∞.
+__device__ __forceinline__ uint64_t logit_key(float v, int e) {
+  v = v != v ? -INFINITY : (v == 0.0f ? 0.0f : v);
+  const uint32_t b = __float_as_uint(v);
+  const uint32_t o = (b & 0x80000000u) ? ~b : (b | 0x80000000u);
+  return ((uint64_t)o << 32) | (uint32_t)(EMAX - 1 - e);
+}
+__device__ __forceinline__ float key_value(uint64_t key) {
+  const uint32_t o = (uint32_t)(key >> 32);
+  return __uint_as_float((o & 0x80000000u) ? (o & 0x7fffffffu) : ~o);
 }
 
-// Stable placement of the slots [s_begin, s_begin + n_slots) by NW waves.
-// off[e]: the global position of this workgroup's first slot of expert e.
-// wrun: NW × EMAX ints of LDS. Ends after writing perm.
-template <int NW>
+// Stable placement of the slots [s_begin, s_begin + n_slots) of one
+// workgroup (n_slots ≤ PLACE_MAX_SLOTS). Each slot sets its bit in its
+// expert's slot mask (LDS atomicOr: the result does not depend on the
+// order); a slot's rank among its expert's slots is then the popcount of
+// the mask below its own bit, so the position off[e] + rank is its place in
+// the sort by (expert, slot id). off[e]: the global position of this
+// workgroup's first slot of expert e. masks: E × PLACE_WORDS words of LDS.
+constexpr int PLACE_MAX_SLOTS = KMAX * ROUTE_TOKENS;
+constexpr int PLACE_WORDS = PLACE_MAX_SLOTS / 32;
+
+template <int NT>
 __device__ __forceinline__ void place_slots(const int32_t* topk_idx, int s_begin, int n_slots, int E,
-                                            const int* off, int (*wrun)[EMAX], int32_t* perm) {
-  constexpr int CH = (KMAX * ROUTE_TOKENS / NW + 63) / 64;     // 64-slot chunks per wave, at most
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int e = threadIdx.x; e < E; e += 64 * NW)
-#pragma unroll
-    for (int w = 0; w < NW; ++w) wrun[w][e] = 0;
+                                            const int* off, uint32_t* masks, int32_t* perm) {
+  constexpr int PER = PLACE_MAX_SLOTS / NT;
+  for (int i = threadIdx.x; i < E * PLACE_WORDS; i += NT) masks[i] = 0u;
   __syncthreads();
-  const int per_wave = (n_slots + NW - 1) / NW;
-  const int s0 = s_begin + wave * per_wave;
-  const int s_end = s_begin + n_slots;
-  const unsigned long long lt = (1ull << lane) - 1ull;
-  int my_e[CH], my_rank[CH];
+  int my_e[PER];
 #pragma unroll
-  for (int c = 0; c < CH; ++c) {
-    my_e[c] = -1;
-    my_rank[c] = 0;
-    if (c * 64 >= per_wave) continue;        // uniform
-    const int s = s0 + c * 64 + lane;
-    const bool valid = (c * 64 + lane < per_wave) && s < s_end;
-    const int e = valid ? topk_idx[s] : -1;
-    my_e[c] = e;
-    unsigned long long pending = __ballot(valid);
-    while (pending) {
-      const int leader = __ffsll((long long)pending) - 1;
-      const int le = __shfl(e, leader, 64);
-      const unsigned long long m = __ballot(valid && e == le);
-      const int run = wrun[wave][le];
-      if (valid && e == le) my_rank[c] = run + __popcll(m & lt);
-      if (lane == leader) wrun[wave][le] = run + __popcll(m);
-      pending &= ~m;
-    }
+  for (int c = 0; c < PER; ++c) {
+    const int sl = threadIdx.x + c * NT;
+    my_e[c] = sl < n_slots ? topk_idx[s_begin + sl] : -1;
+    if (my_e[c] >= 0) atomicOr(&masks[my_e[c] * PLACE_WORDS + (sl >> 5)], 1u << (sl & 31));
   }
   __syncthreads();
 #pragma unroll
-  for (int c = 0; c < CH; ++c) {
+  for (int c = 0; c < PER; ++c) {
     const int e = my_e[c];
     if (e < 0) continue;
-    int r = off[e] + my_rank[c];
-    for (int w = 0; w < wave; ++w) r += wrun[w][e];
-    perm[r] = s0 + c * 64 + lane;
+    const int sl = threadIdx.x + c * NT;
+    const uint32_t* m = masks + e * PLACE_WORDS;
+    int rank = __popc(m[sl >> 5] & ((1u << (sl & 31)) - 1u));
+    for (int w = 0; w < (sl >> 5); ++w) rank += __popc(m[w]);
+    perm[off[e] + rank] = s_begin + sl;
   }
 }
 
-// Exclusive prefix of the per-expert totals `tot` (in place) by one thread;
-// workgroup 0 also publishes offsets and the m-tile prefix.
+// Exclusive prefix of the per-expert totals `tot` (in place) and of their
+// m-tile counts, by wave 0: lane l owns experts 4l .. 4l + 3 (E ≤ 256), then a
+// wave-wide scan of the lane sums. Workgroup 0 also publishes offsets and
+// the m-tile prefix.
 __device__ __forceinline__ void publish_offsets(int* tot, int E, int BM, int32_t* offsets, int32_t* tile_off) {
-  if (threadIdx.x == 0) {
-    int acc = 0, tacc = 0;
-    for (int e = 0; e < E; ++e) {
-      const int c = tot[e];
-      tot[e] = acc;
-      if (blockIdx.x == 0) {
-        offsets[e] = acc;
-        tile_off[e] = tacc;
-      }
-      acc += c;
-      tacc += (c + BM - 1) / BM;
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
+    int c[4], tc[4], s = 0, ts = 0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = 4 * lane + q;
+      c[q] = e < E ? tot[e] : 0;
+      tc[q] = (c[q] + BM - 1) / BM;
+      s += c[q];
+      ts += tc[q];
     }
-    if (blockIdx.x == 0) {
-      offsets[E] = acc;
-      tile_off[E] = tacc;
+    int incl = s, tincl = ts;
+#pragma unroll
+    for (int d = 1; d < 64; d <<= 1) {
+      const int y = __shfl_up(incl, d, 64), ty = __shfl_up(tincl, d, 64);
+      if (lane >= d) {
+        incl += y;
+        tincl += ty;
+      }
+    }
+    int acc = incl - s, tacc = tincl - ts;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = 4 * lane + q;
+      if (e < E) {
+        tot[e] = acc;
+        if (blockIdx.x == 0) {
+          offsets[e] = acc;
+          tile_off[e] = tacc;
+        }
+      }
+      acc += c[q];
+      tacc += tc[q];
+    }
+    if (blockIdx.x == 0 && lane == 63) {
+      offsets[E] = incl;
+      tile_off[E] = tincl;
     }
   }
   __syncthreads();
@@ -138,7 +161,7 @@ __global__ __launch_bounds__(64 * ROUTE_WAVES) void moe_route_kernel(const float
   // row pitch E + 1 floats: thread t reading its row's logit e hits bank (t·(E+1) + e) mod 64
   __shared__ float lg[ROUTE_TOKENS * (EMAX + 1)];
   __shared__ int hist[EMAX];
-  __shared__ int wrun[FUSED_PLACE ? ROUTE_WAVES : 1][EMAX];
+  __shared__ uint32_t masks[FUSED_PLACE ? EMAX * PLACE_WORDS : 1];
   const int t0 = blockIdx.x * ROUTE_TOKENS;
   const int nt = T - t0 < ROUTE_TOKENS ? T - t0 : ROUTE_TOKENS;
   const int pitch = E + 1;
@@ -160,48 +183,66 @@ __global__ __launch_bounds__(64 * ROUTE_WAVES) void moe_route_kernel(const float
     }
   }
   __syncthreads();
-  const int tt = threadIdx.x;
-  if (tt < nt) {
-    // insertion into a list sorted by (value descending, index ascending);
-    // experts arrive in ascending order, an entry is displaced only by a
-    // larger key, and the compare-exchange is branch-free
-    float bv[KMAX];
-    int bi[KMAX];
+  // four lanes per token: lane `sub` scans experts sub, sub + 4, ...; each
+  // pass takes the largest key below the previous winner, as a max over the
+  // lane's keys followed by a max over the quad
+  const int tt = threadIdx.x >> 2, sub = threadIdx.x & 3;
+  const bool active = tt < nt;
+  const float* row = lg + (active ? tt : 0) * pitch;
+  uint64_t win = ~0ull;
+  int sel_i = -1;           // lane q of the quad keeps selection q (and q + 4)
+  int sel_i2 = -1;
+  float sel_v = -INFINITY, sel_v2 = -INFINITY, top = -INFINITY;
+  for (int j = 0; j < k; ++j) {
+    uint64_t part[4] = {0, 0, 0, 0};
+    for (int e0 = sub; e0 < E; e0 += 16) {
 #pragma unroll
-    for (int p = 0; p < KMAX; ++p) {
-      bv[p] = -INFINITY;
-      bi[p] = -1;
-    }
-    const float* row = lg + tt * pitch;
-    for (int e = 0; e < E; ++e) {
-      const float x = row[e];
-      float v = x != x ? -INFINITY : x;     // a NaN logit ranks as −∞, so k experts are always selected
-      int id = e;
-#pragma unroll
-      for (int p = 0; p < KMAX; ++p) {
-        const bool take = (bi[p] < 0) | key_wins(v, id, bv[p], bi[p]);
-        const float nv = take ? v : bv[p];
-        const int ni = take ? id : bi[p];
-        v = take ? bv[p] : v;
-        id = take ? bi[p] : id;
-        bv[p] = nv;
-        bi[p] = ni;
+      for (int u = 0; u < 4; ++u) {
+        const int e = e0 + 4 * u;
+        if (e < E) {
+          const uint64_t key = logit_key(row[e], e);
+          part[u] = (key < win && key > part[u]) ? key : part[u];
+        }
       }
     }
-    float ex[KMAX], sum = 0.0f;
+    uint64_t m = part[0] > part[1] ? part[0] : part[1];
+    const uint64_t m2 = part[2] > part[3] ? part[2] : part[3];
+    m = m > m2 ? m : m2;
 #pragma unroll
-    for (int p = 0; p < KMAX; ++p) {
-      ex[p] = p < k ? expf(bv[p] - bv[0]) : 0.0f;
-      sum += ex[p];
+    for (int d = 1; d <= 2; d <<= 1) {
+      const uint32_t lo = __shfl_xor((uint32_t)m, d, 64), hi = __shfl_xor((uint32_t)(m >> 32), d, 64);
+      const uint64_t o = ((uint64_t)hi << 32) | lo;
+      m = o > m ? o : m;
     }
+    win = m;
+    const int e = EMAX - 1 - (int)(win & 0xffffffffu);
+    const float v = key_value(win);
+    if (j == 0) top = v;
+    if (j == sub) {
+      sel_i = e;
+      sel_v = v;
+    }
+    if (j == sub + 4) {
+      sel_i2 = e;
+      sel_v2 = v;
+    }
+  }
+  const float ex = sub < k ? expf(sel_v - top) : 0.0f;
+  const float ex2 = sub + 4 < k ? expf(sel_v2 - top) : 0.0f;
+  float sum = ex + ex2;
+#pragma unroll
+  for (int d = 1; d <= 2; d <<= 1) sum += __shfl_xor(sum, d, 64);
+  if (active) {
     const int t = t0 + tt;
-#pragma unroll
-    for (int p = 0; p < KMAX; ++p) {
-      if (p < k) {
-        topk_idx[(int64_t)t * k + p] = bi[p];
-        topk_w[(int64_t)t * k + p] = ex[p] / sum;
-        atomicAdd(&hist[bi[p]], 1);
-      }
+    if (sub < k) {
+      topk_idx[(int64_t)t * k + sub] = sel_i;
+      topk_w[(int64_t)t * k + sub] = ex / sum;
+      atomicAdd(&hist[sel_i], 1);
+    }
+    if (sub + 4 < k) {
+      topk_idx[(int64_t)t * k + sub + 4] = sel_i2;
+      topk_w[(int64_t)t * k + sub + 4] = ex2 / sum;
+      atomicAdd(&hist[sel_i2], 1);
     }
   }
   __syncthreads();
@@ -209,7 +250,7 @@ __global__ __launch_bounds__(64 * ROUTE_WAVES) void moe_route_kernel(const float
     // the only workgroup: its histogram is the total; topk_idx written above
     // by this workgroup is visible after the barrier
     publish_offsets(hist, E, BM, offsets, tile_off);
-    place_slots<ROUTE_WAVES>(topk_idx, 0, T * k, E, hist, wrun, perm);
+    place_slots<64 * ROUTE_WAVES>(topk_idx, 0, T * k, E, hist, masks, perm);
   } else {
     for (int e = threadIdx.x; e < E; e += 64 * ROUTE_WAVES) block_counts[(int64_t)blockIdx.x * E + e] = hist[e];
   }
@@ -221,7 +262,7 @@ __global__ __launch_bounds__(64 * PLACE_WAVES) void moe_place_kernel(const int32
                                                                      int32_t* perm) {
   __shared__ int tot[EMAX];
   __shared__ int before[EMAX];
-  __shared__ int wrun[PLACE_WAVES][EMAX];
+  __shared__ uint32_t masks[EMAX * PLACE_WORDS];
   for (int e = threadIdx.x; e < E; e += 64 * PLACE_WAVES) {
     tot[e] = 0;
     before[e] = 0;
@@ -253,7 +294,7 @@ __global__ __launch_bounds__(64 * PLACE_WAVES) void moe_place_kernel(const int32
   __syncthreads();
   const int s_begin = blockIdx.x * ROUTE_TOKENS * k;
   const int n_slots = (S - s_begin) < ROUTE_TOKENS * k ? S - s_begin : ROUTE_TOKENS * k;
-  place_slots<PLACE_WAVES>(topk_idx, s_begin, n_slots, E, before, wrun, perm);
+  place_slots<64 * PLACE_WAVES>(topk_idx, s_begin, n_slots, E, before, masks, perm);
 }
 
 // ---------------------------------------------------------------------------
@@ -311,12 +352,18 @@ __device__ __forceinline__ int64_t weight_row(const GroupedArgs& a, int tn, int 
 template <class TL, int EPI>
 __global__ __launch_bounds__(TL::THREADS) void grouped_kernel(GroupedArgs a) {
   __shared__ __attribute__((aligned(16))) char lds[GroupedLds<TL>::BYTES];
-  // n fastest; with tiles_n_grid a multiple of 8 and workgroups dealt to the
-  // 8 XCDs round-robin, every m-tile of a given n-tile runs on the same XCD,
-  // so the weight tile is fetched into one L2 and reused there
-  const int tn = blockIdx.x % a.tiles_n_grid;
-  const int mt = blockIdx.x / a.tiles_n_grid;
-  if (tn >= a.tiles_n || mt >= a.tile_off[a.E]) return;
+  // Persistent tile loop: workgroup b takes tiles b, b + G, b + 2G, ...
+  // (G = gridDim.x, a multiple of 8) up to the tile count read from the
+  // device-side m-tile prefix, which every workgroup reaches. Tile t is
+  // (m-tile t / tiles_n_grid, n-tile t % tiles_n_grid), n fastest; with
+  // tiles_n_grid and G multiples of 8 and workgroups dealt to the 8 XCDs
+  // round-robin, every m-tile of a given n-tile runs on the same XCD, so the
+  // weight tile is fetched into one L2 and reused there.
+  const int ntiles = a.tile_off[a.E] * a.tiles_n_grid;
+  for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
+  const int tn = t % a.tiles_n_grid;
+  const int mt = t / a.tiles_n_grid;
+  if (tn >= a.tiles_n) continue;
   int lo = 0, hi = a.E;        // tile_off[lo] ≤ mt < tile_off[hi]
   while (hi - lo > 1) {
     const int mid = (lo + hi) >> 1;
@@ -413,6 +460,9 @@ __global__ __launch_bounds__(TL::THREADS) void grouped_kernel(GroupedArgs a) {
           return row < seg1 ? out + ((int64_t)a.perm[row] * ldo + n0) * 2 : nullptr;
         },
         ncols);
+  }
+  // the next tile's loads overwrite the LDS this tile's store just read
+  __syncthreads();
   }
 }
 
@@ -528,13 +578,43 @@ static fg_status validate_desc(const moe_desc* d, const char* fn) {
 
 // n-tiles: gate/up tiles cover BN/2 columns of h (BN weight rows, gate and
 // up interleaved), down tiles BN columns of the output.
+// Resident workgroups of a kernel on the current device (occupancy × CUs),
+// queried once per kernel and device.
+template <class TL, int EPI>
+static int resident_workgroups() {
+  static int cached[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int per_cu = 0, cus = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, grouped_kernel<TL, EPI>, TL::THREADS, 0) != hipSuccess ||
+        per_cu < 1)
+      per_cu = 1;
+    if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) cus = 256;
+    cached[dev] = per_cu * cus;
+  }
+  return cached[dev];
+}
+
 template <class TL, int EPI>
 static void launch_grouped(GroupedArgs a, int64_t S, hipStream_t s) {
   a.tiles_n = EPI == EPI_GATEUP ? (int)(a.I / (TL::BN / 2)) : (int)((a.Nw + TL::BN - 1) / TL::BN);
   a.tiles_n_grid = (a.tiles_n + 7) / 8 * 8;
+  // the m-tile count is known only on the device; its upper bound is
+  // Σ_e ceil(n_e / BM) ≤ (S + E·(BM − 1)) / BM
   const int64_t mtiles = (S + (int64_t)a.E * (TL::BM - 1)) / TL::BM;
-  const unsigned grid = (unsigned)(mtiles * a.tiles_n_grid);
-  hipLaunchKernelGGL((grouped_kernel<TL, EPI>), dim3(grid), dim3(TL::THREADS), 0, s, a);
+  const int64_t upper = mtiles * a.tiles_n_grid;
+  // Small (decode) tiles stream weights: size the grid to the resident
+  // workgroups so that no partial last wave of workgroups idles the chip.
+  // Large (prefill) tiles keep one tile per workgroup, which measured ~5 %
+  // faster than the persistent loop there.
+  int64_t grid = upper;
+  if (TL::BM <= 32) {
+    const int64_t res = resident_workgroups<TL, EPI>();
+    grid = res < upper ? res : upper;
+  }
+  grid = grid / 8 * 8 > 0 ? grid / 8 * 8 : 8;
+  hipLaunchKernelGGL((grouped_kernel<TL, EPI>), dim3((unsigned)grid), dim3(TL::THREADS), 0, s, a);
 }
 
 }  // namespace fg
