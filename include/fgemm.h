@@ -115,8 +115,10 @@ typedef struct fg_plan fg_plan; /* opaque, host memory, immutable once built */
 fg_status fgemm_plan(fg_plan **plan, int64_t M, int64_t N, int64_t K,
                      int32_t in_dtype, int32_t out_dtype, const fg_epilogue *epi);
 
-/* Bytes of device workspace fgemm_run needs (the LogSumExp per-tile
- * (max, Σexp) partials; 0 for the other tails). 0 for a NULL plan. */
+/* Bytes of device workspace fgemm_run needs: the LogSumExp per-tile
+ * (max, Σexp) pairs, and, when the plan splits K across workgroups, one
+ * arrival counter per output tile plus an fp32 partial tile per slice. 0 when
+ * neither applies, and for a NULL plan. */
 size_t fgemm_workspace_bytes(const fg_plan *plan);
 
 /*
@@ -126,7 +128,10 @@ size_t fgemm_workspace_bytes(const fg_plan *plan);
  *   gamma, beta  [N] fp32, required iff GroupNorm (else ignored).
  *   out    [M, N] out_dtype, or [M] fp32 for LogSumExp.
  *   workspace, ws_bytes  device scratch of at least fgemm_workspace_bytes;
- *          may be NULL when that is 0. Contents on entry are ignored.
+ *          may be NULL when that is 0. Contents on entry are ignored: the
+ *          split-K arrival counters carry a per-run epoch, so values left by
+ *          other runs or by other users of the memory are recognised as
+ *          stale. Runs that overlap in time must not share a workspace.
  * Re-entrant: one plan may be run concurrently on several streams provided
  * each run has its own output and workspace.
  */
@@ -137,10 +142,11 @@ fg_status fgemm_run(const fg_plan *plan, const void *A, const void *W,
 void fgemm_destroy(fg_plan *plan);
 
 /* Kernel choice of a plan, for tests and reports: tile rows and columns,
- * workgroups per launch, and launches per run. Returns FG_ERR_INVALID_ARG
- * for a NULL plan. Any output pointer may be NULL. */
+ * workgroups per launch, launches per run, and K slices (1 unless the plan
+ * splits K across workgroups). Returns FG_ERR_INVALID_ARG for a NULL plan.
+ * Any output pointer may be NULL. */
 fg_status fgemm_plan_info(const fg_plan *plan, int32_t *tile_m, int32_t *tile_n,
-                          int64_t *workgroups, int32_t *launches);
+                          int64_t *workgroups, int32_t *launches, int32_t *k_slices);
 
 /* ---------------------------------------------------------------------- */
 /* MoE expert FFN                                                         */

@@ -64,7 +64,8 @@ def lib():
         L.fgemm_run.restype = i32
         L.fgemm_destroy.argtypes = [vp]
         L.fgemm_destroy.restype = None
-        L.fgemm_plan_info.argtypes = [vp, C.POINTER(i32), C.POINTER(i32), C.POINTER(i64), C.POINTER(i32)]
+        L.fgemm_plan_info.argtypes = [vp, C.POINTER(i32), C.POINTER(i32), C.POINTER(i64), C.POINTER(i32),
+                                      C.POINTER(i32)]
         L.fgemm_plan_info.restype = i32
         L.moe_workspace_bytes.argtypes = [C.POINTER(MoeDesc)]
         L.moe_workspace_bytes.restype = sz
@@ -127,10 +128,11 @@ class Plan:
         return fgemm_workspace_bytes(self)
 
     def info(self):
-        tm, tn, wg, nl = C.c_int32(), C.c_int32(), C.c_int64(), C.c_int32()
-        _check(lib().fgemm_plan_info(self.handle, C.byref(tm), C.byref(tn), C.byref(wg), C.byref(nl)),
-               "fgemm_plan_info")
-        return {"tile_m": tm.value, "tile_n": tn.value, "workgroups": wg.value, "launches": nl.value}
+        tm, tn, wg, nl, ks = C.c_int32(), C.c_int32(), C.c_int64(), C.c_int32(), C.c_int32()
+        _check(lib().fgemm_plan_info(self.handle, C.byref(tm), C.byref(tn), C.byref(wg), C.byref(nl),
+                                     C.byref(ks)), "fgemm_plan_info")
+        return {"tile_m": tm.value, "tile_n": tn.value, "workgroups": wg.value, "launches": nl.value,
+                "k_slices": ks.value}
 
     def close(self):
         if self._h:

@@ -25,15 +25,17 @@ struct EpiArgs {
   float b[FG_MAX_OPS];
 };
 
-// GELU, tanh form: ½u(1 + tanh(√(2/π)(u + 0.044715u³))).
+// GELU, tanh form: ½u(1 + tanh(z)) with z = √(2/π)(u + 0.044715u³). Since
+// ½(1 + tanh z) = σ(2z), this is u·σ(2z): one exponential and one
+// reciprocal instead of a tanh.
 __device__ __forceinline__ float gelu_tanh(float u) {
-  const float k0 = 0.7978845608028654f;  // √(2/π)
+  const float k0 = 2.0f * 0.7978845608028654f;  // 2·√(2/π)
   const float k1 = 0.044715f;
-  return 0.5f * u * (1.0f + tanhf(k0 * (u + k1 * u * u * u)));
+  return u * fast_sigmoid(k0 * (u + k1 * u * u * u));
 }
 
-// SiLU u·σ(u) = u/(1 + e^−u); for u → −∞ the quotient tends to −0.
-__device__ __forceinline__ float silu(float u) { return u / (1.0f + expf(-u)); }
+// SiLU u·σ(u); for u → −∞ it tends to −0.
+__device__ __forceinline__ float silu(float u) { return u * fast_sigmoid(u); }
 
 // The chain runs over one block of FN·4 accumulators at a time (one fm),
 // all ops on that block before the next, so only that block is live in
@@ -125,7 +127,7 @@ __device__ __forceinline__ void lse_partials(f32x4 (&acc)[TL::FM][TL::FN], float
       float s = 0.0f;
 #pragma unroll
       for (int fn = 0; fn < TL::FN; ++fn)
-        if (colok[fn]) s += expf(acc[fm][fn][i] - mx);
+        if (colok[fn]) s += fast_exp(acc[fm][fn][i] - mx);
       s = row16_sum(s);
       if ((l & 15) == 0) rsum[wn * TL::BM + r] = s;
     }
@@ -209,7 +211,7 @@ __device__ __forceinline__ void groupnorm_tile(f32x4 (&acc)[TL::FM][TL::FN], flo
 #pragma unroll
       for (int w = 0; w < TL::WN; ++w)
         if ((w * TL::TN) / gw == my_group) s += red[w * TL::BM + r];
-      const float rstd = 1.0f / sqrtf(s * inv_gw + eps);
+      const float rstd = fast_rsqrt(s * inv_gw + eps);
 #pragma unroll
       for (int fn = 0; fn < TL::FN; ++fn)
         acc[fm][fn][i] = (acc[fm][fn][i] - mean[fm][i]) * rstd * gm[fn] + bt[fn];

@@ -64,135 +64,240 @@ __device__ __forceinline__ int lds_off(int row, int chunk) {
 }
 
 // Row sources for the stage loads. Thread t owns tile rows
-// (t >> 3) + (THREADS/8)·p, p < NLD; `ptr[p]` is the start of that row in global
-// memory. Rows past the matrix edge point at any valid row: their LDS copy
+// r = (t >> 3) + (THREADS/8)·p, p < NLD. Two sources implement the same two
+// operations:
+//   stage(kbyte, sbase)        direct HBM → LDS load of one full stage;
+//   tail(kbyte, kbytes, sbase) zero-filling load of a partial last stage.
+// The direct loads write lane i's 16 bytes at LDS offset 16·i of a
+// wave-uniform 1 KiB block, i.e. block b = wave + NWAVES·p holds tile rows
+// 8b .. 8b + 7 with physical chunk i & 7; the lane therefore fetches logical
+// chunk (i & 7) ^ (i >> 3), the inverse of the LDS swizzle.
+
+// Gathered rows (MoE token rows through the permutation): one pointer per
+// owned row. Rows past the matrix edge point at any valid row: their LDS copy
 // only feeds accumulator rows / columns that are never stored.
 template <int NLD>
 struct RowSet {
   const char* ptr[NLD];
+
+  template <int NWAVES>
+  __device__ __forceinline__ void stage(int64_t kbyte, char* sbase) const {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int c = (lane & 7) ^ (lane >> 3);
+#pragma unroll
+    for (int p = 0; p < NLD; ++p) {
+      const char* src = ptr[p] + kbyte + c * 16;
+      char* dst = sbase + (wave + NWAVES * p) * 1024;
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(src),
+                                       (__attribute__((address_space(3))) void*)(dst), 16, 0, 0);
+    }
+  }
+
+  template <int RSTRIDE>
+  __device__ __forceinline__ void tail(int64_t kbyte, int64_t kbytes, char* sbase) const {
+    const int c = threadIdx.x & 7;
+    const int r0 = threadIdx.x >> 3;
+    const int64_t off = kbyte + c * 16;
+#pragma unroll
+    for (int p = 0; p < NLD; ++p) {
+      i32x4 v = {0, 0, 0, 0};
+      if (off < kbytes) v = *reinterpret_cast<const i32x4*>(ptr[p] + off);
+      *reinterpret_cast<i32x4*>(sbase + lds_off(r0 + RSTRIDE * p, c)) = v;
+    }
+  }
 };
 
-// Direct HBM → LDS load of one full stage (every row has 128 valid bytes at
-// kbyte): global_load_lds_dwordx4 writes lane i's 16 bytes at LDS offset
-// 16·i of a wave-uniform 1 KiB block, i.e. block b = wave + NWAVES·p holds
-// tile rows 8b .. 8b + 7 with physical chunk i & 7. The lane therefore
-// fetches logical chunk (i & 7) ^ (i >> 3), the inverse of the LDS swizzle.
-template <int NWAVES, int NLD>
-__device__ __forceinline__ void load_stage_direct(const RowSet<NLD>& rs, int64_t kbyte, char* sbase) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int c = (lane & 7) ^ (lane >> 3);
-#pragma unroll
-  for (int p = 0; p < NLD; ++p) {
-    const char* src = rs.ptr[p] + kbyte + c * 16;
-    char* dst = sbase + (wave + NWAVES * p) * 1024;
-    __builtin_amdgcn_global_load_lds(static_cast<const void*>(src),
-                                     (__attribute__((address_space(3))) void*)(dst), 16, 0, 0);
-  }
+// Buffer-resource loads (MUBUF with the LDS bit, and a 128-bit MUBUF load for
+// the tail), bound to the LLVM intrinsics. Offsets beyond num_records read
+// as zero, which is how rows past the matrix edge are filled.
+__device__ void fg_raw_buffer_load_lds(i32x4 rsrc, __attribute__((address_space(3))) void* lds, uint32_t size,
+                                       uint32_t voffset, uint32_t soffset, uint32_t offset,
+                                       uint32_t aux) __asm("llvm.amdgcn.raw.buffer.load.lds");
+__device__ i32x4 fg_raw_buffer_load_b128(i32x4 rsrc, uint32_t voffset, uint32_t soffset,
+                                         uint32_t aux) __asm("llvm.amdgcn.raw.buffer.load.v4i32");
+__device__ void fg_raw_buffer_store_b128(i32x4 data, i32x4 rsrc, uint32_t voffset, uint32_t soffset,
+                                         uint32_t aux) __asm("llvm.amdgcn.raw.buffer.store.v4i32");
+// Cache-policy bit of the buffer intrinsics that makes an access device
+// coherent (sc1 on gfx950: a store writes through to the device coherence
+// point, a load does not hit a stale line), as for agent-scope atomics.
+constexpr uint32_t FG_CPOL_DEVICE = 16;
+
+// 128-bit buffer descriptor: 48-bit base, stride 0 (raw), num_records bytes,
+// and the data-format word used for untyped raw access on gfx9-class parts.
+__device__ __forceinline__ i32x4 make_buffer_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t b = reinterpret_cast<uint64_t>(base);
+  return i32x4{static_cast<int>(static_cast<uint32_t>(b)), static_cast<int>(static_cast<uint32_t>(b >> 32) & 0xffff),
+               static_cast<int>(bytes), 0x00020000};
 }
 
-// Zero-filling load of a partial stage through VGPRs: chunks at or past
-// kbytes read as zero, so the tail contributes nothing beyond K.
-template <int RSTRIDE, int NLD>
-__device__ __forceinline__ void load_stage_tail(const RowSet<NLD>& rs, int64_t kbyte, int64_t kbytes,
-                                                char* sbase) {
-  const int c = threadIdx.x & 7;
-  const int r0 = threadIdx.x >> 3;
-  const int64_t off = kbyte + c * 16;
-#pragma unroll
-  for (int p = 0; p < NLD; ++p) {
-    i32x4 v = {0, 0, 0, 0};
-    if (off < kbytes) v = *reinterpret_cast<const i32x4*>(rs.ptr[p] + off);
-    *reinterpret_cast<i32x4*>(sbase + lds_off(r0 + RSTRIDE * p, c)) = v;
+// Strided rows (dense x and W tiles): row r of the tile is at base + r·stride.
+// The descriptor covers the tile's valid rows only, so rows past the matrix
+// edge load as zeros. Every offset stays below 2^31 (the plan bounds
+// BM·stride), and each lane keeps one 32-bit offset instead of NLD pointers.
+template <int NLD, int RSTRIDE>
+struct BufRows {
+  i32x4 rsrc;         // wave-uniform
+  uint32_t voff;      // (t >> 3)·stride + 16·(fetched chunk)
+  uint32_t pstride;   // RSTRIDE·stride
+  uint32_t stride;
+
+  __device__ __forceinline__ void init(const char* base, int64_t rows_valid, int64_t rows_tile, int64_t row_stride) {
+    const int64_t rows = rows_valid < rows_tile ? rows_valid : rows_tile;
+    rsrc = make_buffer_rsrc(base, static_cast<uint32_t>(rows * row_stride));
+    stride = static_cast<uint32_t>(row_stride);
+    pstride = static_cast<uint32_t>(RSTRIDE * row_stride);
+    const int lane = threadIdx.x & 63;
+    voff = static_cast<uint32_t>(threadIdx.x >> 3) * stride + static_cast<uint32_t>(((lane & 7) ^ (lane >> 3)) * 16);
   }
-}
+
+  template <int NWAVES>
+  __device__ __forceinline__ void stage(int64_t kbyte, char* sbase) const {
+    const int wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int p = 0; p < NLD; ++p) {
+      char* dst = sbase + (wave + NWAVES * p) * 1024;
+      fg_raw_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(dst), 16,
+                             voff + p * pstride + static_cast<uint32_t>(kbyte), 0, 0, 0);
+    }
+  }
+
+  template <int RS>
+  __device__ __forceinline__ void tail(int64_t kbyte, int64_t kbytes, char* sbase) const {
+    const int c = threadIdx.x & 7;
+    const int r0 = threadIdx.x >> 3;
+    const int64_t off = kbyte + c * 16;
+    const uint32_t rowoff = static_cast<uint32_t>(r0) * stride + static_cast<uint32_t>(off);
+#pragma unroll
+    for (int p = 0; p < NLD; ++p) {
+      i32x4 v = {0, 0, 0, 0};
+      if (off < kbytes) v = fg_raw_buffer_load_b128(rsrc, rowoff + p * pstride, 0, 0);
+      *reinterpret_cast<i32x4*>(sbase + lds_off(r0 + RS * p, c)) = v;
+    }
+  }
+};
 
 __device__ __forceinline__ void wait_vmem() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
-// acc[fm][fn] += A-fragments × B-fragments for one LDS stage.
+// Operand fragments of one substep. A stage is split into SUB substeps:
+// bf16 and fp32 take chunk 2g + h in substep h (h = 0, 1), so one substep is
+// one 16×16×32 bf16 MFMA (or four 16×16×4 fp32 MFMAs) per fragment pair;
+// e4m3 needs both chunks 2g, 2g + 1 for its single 16×16×128 MFMA, so its
+// stage is one substep.
+template <class TL, In IN = TL::IN> struct Frag;
+template <class TL> struct Frag<TL, In::BF16> { static constexpr int SUB = 2; using V = bf16x8; V a[TL::FM], b[TL::FN]; };
+template <class TL> struct Frag<TL, In::F32>  { static constexpr int SUB = 2; using V = f32x4; V a[TL::FM], b[TL::FN]; };
+template <class TL> struct Frag<TL, In::E4M3> { static constexpr int SUB = 1; using V = i32x8; V a[TL::FM], b[TL::FN]; };
+
 template <class TL>
-__device__ __forceinline__ void mma_stage(const char* sA, const char* sB, int wm, int wn,
-                                          f32x4 (&acc)[TL::FM][TL::FN]) {
+__device__ __forceinline__ i32x4 lds16(const char* stage, int row, int chunk) {
+  return *reinterpret_cast<const i32x4*>(stage + lds_off(row, chunk));
+}
+
+// Read substep h of the stage at `sA` (B rows follow the BM A rows).
+template <class TL>
+__device__ __forceinline__ void read_frag(const char* sA, int wm, int wn, int h, Frag<TL>& F) {
+  const char* sB = sA + TL::BM * TL::ROWB;
   const int l = threadIdx.x & 63;
-  const int g = l >> 4;
-  const int r16 = l & 15;
-  if constexpr (TL::IN == In::BF16) {
+  const int g = l >> 4, r16 = l & 15;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      bf16x8 af[TL::FM], bfr[TL::FN];
-#pragma unroll
-      for (int fm = 0; fm < TL::FM; ++fm) {
-        const int r = wm * TL::TM + fm * 16 + r16;
-        af[fm] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const i32x4*>(sA + lds_off(r, 2 * g + h)));
-      }
-#pragma unroll
-      for (int fn = 0; fn < TL::FN; ++fn) {
-        const int r = wn * TL::TN + fn * 16 + r16;
-        bfr[fn] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const i32x4*>(sB + lds_off(r, 2 * g + h)));
-      }
-#pragma unroll
-      for (int fm = 0; fm < TL::FM; ++fm)
-#pragma unroll
-        for (int fn = 0; fn < TL::FN; ++fn)
-          acc[fm][fn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[fm], bfr[fn], acc[fm][fn], 0, 0, 0);
-    }
-  } else if constexpr (TL::IN == In::E4M3) {
-    i32x8 af[TL::FM], bfr[TL::FN];
-#pragma unroll
-    for (int fm = 0; fm < TL::FM; ++fm) {
-      const int r = wm * TL::TM + fm * 16 + r16;
-      const i32x4 lo = *reinterpret_cast<const i32x4*>(sA + lds_off(r, 2 * g));
-      const i32x4 hi = *reinterpret_cast<const i32x4*>(sA + lds_off(r, 2 * g + 1));
-      af[fm] = i32x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-    }
-#pragma unroll
-    for (int fn = 0; fn < TL::FN; ++fn) {
-      const int r = wn * TL::TN + fn * 16 + r16;
-      const i32x4 lo = *reinterpret_cast<const i32x4*>(sB + lds_off(r, 2 * g));
-      const i32x4 hi = *reinterpret_cast<const i32x4*>(sB + lds_off(r, 2 * g + 1));
-      bfr[fn] = i32x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-    }
-#pragma unroll
-    for (int fm = 0; fm < TL::FM; ++fm)
-#pragma unroll
-      for (int fn = 0; fn < TL::FN; ++fn)
-        // operand formats 0 = FP8 E4M3 for A and B; E8M0 scale 127 = 2^0
-        acc[fm][fn] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(
-            af[fm], bfr[fn], acc[fm][fn], 0, 0, 0, 127, 0, 127);
-  } else {
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      f32x4 af[TL::FM], bfr[TL::FN];
-#pragma unroll
-      for (int fm = 0; fm < TL::FM; ++fm) {
-        const int r = wm * TL::TM + fm * 16 + r16;
-        af[fm] = __builtin_bit_cast(f32x4, *reinterpret_cast<const i32x4*>(sA + lds_off(r, 2 * g + h)));
-      }
-#pragma unroll
-      for (int fn = 0; fn < TL::FN; ++fn) {
-        const int r = wn * TL::TN + fn * 16 + r16;
-        bfr[fn] = __builtin_bit_cast(f32x4, *reinterpret_cast<const i32x4*>(sB + lds_off(r, 2 * g + h)));
-      }
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int fm = 0; fm < TL::FM; ++fm)
-#pragma unroll
-          for (int fn = 0; fn < TL::FN; ++fn)
-            acc[fm][fn] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[fm][s], bfr[fn][s], acc[fm][fn], 0, 0, 0);
+  for (int fm = 0; fm < TL::FM; ++fm) {
+    const int r = wm * TL::TM + fm * 16 + r16;
+    if constexpr (TL::IN == In::E4M3) {
+      const i32x4 lo = lds16<TL>(sA, r, 2 * g), hi = lds16<TL>(sA, r, 2 * g + 1);
+      F.a[fm] = i32x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    } else {
+      F.a[fm] = __builtin_bit_cast(typename Frag<TL>::V, lds16<TL>(sA, r, 2 * g + h));
     }
   }
+#pragma unroll
+  for (int fn = 0; fn < TL::FN; ++fn) {
+    const int r = wn * TL::TN + fn * 16 + r16;
+    if constexpr (TL::IN == In::E4M3) {
+      const i32x4 lo = lds16<TL>(sB, r, 2 * g), hi = lds16<TL>(sB, r, 2 * g + 1);
+      F.b[fn] = i32x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+    } else {
+      F.b[fn] = __builtin_bit_cast(typename Frag<TL>::V, lds16<TL>(sB, r, 2 * g + h));
+    }
+  }
+}
+
+// acc[fm][fn] += A-fragment × B-fragment for one substep.
+template <class TL>
+__device__ __forceinline__ void mma_frag(const Frag<TL>& F, f32x4 (&acc)[TL::FM][TL::FN]) {
+#pragma unroll
+  for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < TL::FN; ++fn) {
+      if constexpr (TL::IN == In::BF16) {
+        acc[fm][fn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(F.a[fm], F.b[fn], acc[fm][fn], 0, 0, 0);
+      } else if constexpr (TL::IN == In::E4M3) {
+        // operand formats 0 = FP8 E4M3 for A and B; E8M0 scale 127 = 2^0
+        acc[fm][fn] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(F.a[fm], F.b[fn], acc[fm][fn], 0, 0,
+                                                                       0, 127, 0, 127);
+      } else {
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+          acc[fm][fn] = __builtin_amdgcn_mfma_f32_16x16x4f32(F.a[fm][s], F.b[fn][s], acc[fm][fn], 0, 0, 0);
+      }
+    }
+}
+
+// Issue order inside a substep: each LDS read of the next substep's
+// fragments goes out right after one MFMA of the current substep, so the
+// reads stream while the matrix core works instead of waiting as one block.
+template <class TL>
+__device__ __forceinline__ void interleave_reads_with_mfma() {
+  constexpr int NRD = (TL::FM + TL::FN) * (TL::IN == In::E4M3 ? 2 : 1);
+  constexpr int NMF = TL::FM * TL::FN * (TL::IN == In::F32 ? 4 : 1);
+  constexpr int PAIRS = NRD < NMF ? NRD : NMF;
+#pragma unroll
+  for (int i = 0; i < PAIRS; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+  }
+  if constexpr (NMF > PAIRS) __builtin_amdgcn_sched_group_barrier(0x008, NMF - PAIRS, 0);
+}
+
+// One substep of the pipelined loop: substep j is in Fc; prepare substep
+// j + 1 in Fn, then multiply Fc. When j + 1 opens stage s = (j + 1) / SUB,
+// the workgroup first waits for stage s to have landed (its loads were
+// issued one stage earlier), synchronises — which also retires every read of
+// stage s − 1 — and issues the direct loads of stage s + 1 into the buffer
+// stage s − 1 used. Loads past the last stage repeat the last stage into
+// that free buffer, which is never read again: the loop body needs no branch.
+template <class TL, class LA, class LB>
+__device__ __forceinline__ void pipelined_substep(int64_t j, int64_t KT, const LA& ra, const LB& rb,
+                                                  char* lds, int wm, int wn, const Frag<TL>& Fc, Frag<TL>& Fn,
+                                                  f32x4 (&acc)[TL::FM][TL::FN]) {
+  constexpr int SUB = Frag<TL>::SUB;
+  const int64_t nx = j + 1;
+  const int64_t s = nx / SUB;
+  const int h = static_cast<int>(nx % SUB);
+  if (h == 0) {
+    wait_vmem();
+    __syncthreads();
+    const int64_t sl = s + 1 < KT ? s + 1 : KT - 1;
+    char* dst = lds + ((s + 1) & 1) * TL::STAGE_BYTES;
+    ra.template stage<TL::NWAVES>(sl * TL::ROWB, dst);
+    rb.template stage<TL::NWAVES>(sl * TL::ROWB, dst + TL::BM * TL::ROWB);
+  }
+  read_frag<TL>(lds + (s & 1) * TL::STAGE_BYTES, wm, wn, h, Fn);
+  mma_frag<TL>(Fc, acc);
+  interleave_reads_with_mfma<TL>();
 }
 
 // The K loop: acc = Σ_k A[rows]·B[rows]ᵀ over kbytes bytes of each row.
 // `lds` must hold TL::LOOP_LDS bytes. A partial last stage (kbytes not a
 // multiple of 128) is loaded first through the zero-filling path; the full
-// stages then stream through the two LDS buffers with direct loads, the
-// loads of stage s + 1 in flight while stage s is multiplied. Ends with a
+// stages then stream through the two LDS buffers with direct loads issued
+// two stages ahead of the MFMAs that consume them, while the fragments of
+// substep j + 1 are read during the MFMAs of substep j. Ends with a
 // barrier, so the caller may reuse the LDS immediately.
-template <class TL>
-__device__ __forceinline__ void gemm_mainloop(const RowSet<TL::A_LD>& ra, const RowSet<TL::B_LD>& rb,
+template <class TL, class LA, class LB>
+__device__ __forceinline__ void gemm_mainloop(const LA& ra, const LB& rb,
                                               int64_t kbytes, char* lds,
                                               f32x4 (&acc)[TL::FM][TL::FN]) {
+  constexpr int SUB = Frag<TL>::SUB;
   const int wave = threadIdx.x >> 6;
   const int wm = wave / TL::WN, wn = wave % TL::WN;
 #pragma unroll
@@ -200,31 +305,72 @@ __device__ __forceinline__ void gemm_mainloop(const RowSet<TL::A_LD>& ra, const 
 #pragma unroll
     for (int fn = 0; fn < TL::FN; ++fn) acc[fm][fn] = f32x4{0.f, 0.f, 0.f, 0.f};
 
+  Frag<TL> F0, F1;
   const int64_t KT = kbytes / TL::ROWB;   // full stages
   if (kbytes % TL::ROWB != 0) {
     char* sb = lds + TL::STAGE_BYTES;
-    load_stage_tail<TL::RSTRIDE, TL::A_LD>(ra, KT * TL::ROWB, kbytes, sb);
-    load_stage_tail<TL::RSTRIDE, TL::B_LD>(rb, KT * TL::ROWB, kbytes, sb + TL::BM * TL::ROWB);
+    ra.template tail<TL::RSTRIDE>(KT * TL::ROWB, kbytes, sb);
+    rb.template tail<TL::RSTRIDE>(KT * TL::ROWB, kbytes, sb + TL::BM * TL::ROWB);
     __syncthreads();
-    mma_stage<TL>(sb, sb + TL::BM * TL::ROWB, wm, wn, acc);
+#pragma unroll
+    for (int h = 0; h < SUB; ++h) {
+      read_frag<TL>(sb, wm, wn, h, F0);
+      mma_frag<TL>(F0, acc);
+    }
     __syncthreads();
   }
   if (KT == 0) return;
-  load_stage_direct<TL::NWAVES, TL::A_LD>(ra, 0, lds);
-  load_stage_direct<TL::NWAVES, TL::B_LD>(rb, 0, lds + TL::BM * TL::ROWB);
+  ra.template stage<TL::NWAVES>(0, lds);
+  rb.template stage<TL::NWAVES>(0, lds + TL::BM * TL::ROWB);
+  if (KT > 1) {
+    char* s1 = lds + TL::STAGE_BYTES;
+    ra.template stage<TL::NWAVES>(TL::ROWB, s1);
+    rb.template stage<TL::NWAVES>(TL::ROWB, s1 + TL::BM * TL::ROWB);
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(TL::A_LD + TL::B_LD) : "memory");
+  } else {
+    wait_vmem();
+  }
+  __syncthreads();
+  if constexpr (SUB == 1) {
+    // e4m3: one substep per stage and 32-byte fragments; a second fragment
+    // set would not fit beside two resident workgroups, so each wave reads
+    // and multiplies in turn and the other workgroup's waves fill the gaps.
+    for (int64_t kt = 0; kt < KT; ++kt) {
+      read_frag<TL>(lds + (kt & 1) * TL::STAGE_BYTES, wm, wn, 0, F0);
+      mma_frag<TL>(F0, acc);
+      wait_vmem();
+      __syncthreads();
+      const int64_t sl = kt + 2 < KT ? kt + 2 : KT - 1;
+      char* dst = lds + (kt & 1) * TL::STAGE_BYTES;
+      ra.template stage<TL::NWAVES>(sl * TL::ROWB, dst);
+      rb.template stage<TL::NWAVES>(sl * TL::ROWB, dst + TL::BM * TL::ROWB);
+    }
+  } else {
+    read_frag<TL>(lds, wm, wn, 0, F0);
+    const int64_t J = KT * SUB;               // substeps
+    int64_t j = 0;
+    for (; j + 2 < J; j += 2) {
+      pipelined_substep<TL>(j, KT, ra, rb, lds, wm, wn, F0, F1, acc);
+      pipelined_substep<TL>(j + 1, KT, ra, rb, lds, wm, wn, F1, F0, acc);
+    }
+    // the last one or two substeps: multiply F0 before reading the final
+    // substep into the same registers (one fragment set live, not two, beside
+    // the accumulators); if the final substep opens the last stage its loads
+    // were issued long ago, so only the barrier is needed
+    mma_frag<TL>(F0, acc);
+    if (J - j == 2) {
+      const int64_t s = (j + 1) / SUB;
+      const int h = static_cast<int>((j + 1) % SUB);
+      if (h == 0) {
+        wait_vmem();
+        __syncthreads();
+      }
+      read_frag<TL>(lds + (s & 1) * TL::STAGE_BYTES, wm, wn, h, F0);
+      mma_frag<TL>(F0, acc);
+    }
+  }
   wait_vmem();
   __syncthreads();
-  for (int64_t kt = 0; kt < KT; ++kt) {
-    char* cur = lds + (kt & 1) * TL::STAGE_BYTES;
-    char* nxt = lds + ((kt + 1) & 1) * TL::STAGE_BYTES;
-    if (kt + 1 < KT) {
-      load_stage_direct<TL::NWAVES, TL::A_LD>(ra, (kt + 1) * TL::ROWB, nxt);
-      load_stage_direct<TL::NWAVES, TL::B_LD>(rb, (kt + 1) * TL::ROWB, nxt + TL::BM * TL::ROWB);
-    }
-    mma_stage<TL>(cur, cur + TL::BM * TL::ROWB, wm, wn, acc);
-    wait_vmem();
-    __syncthreads();
-  }
 }
 
 // Position of accumulator element (fm, fn, i) inside the workgroup tile.
@@ -247,17 +393,40 @@ __device__ __forceinline__ float bf16_bits_to_f32(uint16_t b) {
   return __builtin_bit_cast(float, static_cast<uint32_t>(b) << 16);
 }
 
-// Reduce over the 16 lanes that share a tile row (lanes with equal l >> 4).
+// Reduce over the 16 lanes that share a tile row (lanes with equal l >> 4,
+// one DPP row). Four DPP steps: lane ^ 1 and lane ^ 2 (quad permutes) give
+// every lane its quad's total, then rotations of the row by 4 and by 8 add
+// the other three quads. The maximum is the same in all 16 lanes; a sum may
+// differ in the last bit between lanes (different association), so callers
+// take lane (l & 15) == 0's value.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
 __device__ __forceinline__ float row16_sum(float v) {
-#pragma unroll
-  for (int m = 1; m < 16; m <<= 1) v += __shfl_xor(v, m, 64);
+  v += dpp_f<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_f<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_f<0x124>(v);  // row_ror:4
+  v += dpp_f<0x128>(v);  // row_ror:8
   return v;
 }
 __device__ __forceinline__ float row16_max(float v) {
-#pragma unroll
-  for (int m = 1; m < 16; m <<= 1) v = fmaxf(v, __shfl_xor(v, m, 64));
+  v = fmaxf(v, dpp_f<0xB1>(v));
+  v = fmaxf(v, dpp_f<0x4E>(v));
+  v = fmaxf(v, dpp_f<0x124>(v));
+  v = fmaxf(v, dpp_f<0x128>(v));
   return v;
 }
+
+// Native-instruction math for the tails (v_exp_f32 = 2^x, v_rcp_f32,
+// v_rsq_f32; each within a few ulp of fp32, far inside the bf16 and fp32
+// output tolerances). e^x = 2^(x·log2 e) underflows to 0 below about −87
+// and overflows to +inf above about 88, which the callers rely on.
+__device__ __forceinline__ float fast_exp(float x) { return __builtin_amdgcn_exp2f(x * 1.4426950408889634f); }
+__device__ __forceinline__ float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+__device__ __forceinline__ float fast_rsqrt(float x) { return __builtin_amdgcn_rsqf(x); }
+// σ(x) = 1/(1 + e^−x): 1 for large x, 0 (through rcp(+inf)) for very negative x.
+__device__ __forceinline__ float fast_sigmoid(float x) { return fast_rcp(1.0f + fast_exp(-x)); }
 
 // Stage the tile through LDS and write it with 16-byte row-contiguous stores.
 // `vals(fm, fn, i, v, c)` returns whether accumulator element (fm, fn, i)

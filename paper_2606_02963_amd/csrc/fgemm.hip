@@ -6,11 +6,19 @@
 // exception is a LogSumExp over a row that spans several N tiles: each tile
 // writes its (max, Σexp) pair and a second launch of one wave per row
 // combines them (the rescaling identity of online softmax, §I).
+//
+// When a problem has too few output tiles to occupy every compute unit with
+// the large 256×256 tile, K is split into KS slices (split-K): every slice
+// workgroup writes its fp32 partial tile to the workspace and counts its
+// arrival on the tile's counter; the workgroup that arrives last adds the
+// partials in slice order and runs the tail, so the tail still sees the
+// complete accumulator and the result does not depend on arrival order.
 #include <hip/hip_runtime.h>
 #include <math.h>
 #include <stdlib.h>
 #include <string.h>
 
+#include <atomic>
 #include <new>
 
 #include "fg_epilogue.hpp"
@@ -40,34 +48,118 @@ struct DenseArgs {
   float2* ws;
   int M, N;
   int64_t K;
-  int tiles_n;
+  int tiles_m, tiles_n;
+  int ks;                 // K slices (1 = no split)
+  int64_t kslice;         // bytes of each row per slice but the last (multiple of 128)
+  unsigned long long* counters;  // [tiles] (epoch << 32 | arrivals) words (split-K only)
+  unsigned epoch;         // this run's epoch (split-K only)
+  f32x4* partials;        // [tiles · ks · FM·FN · THREADS] partial tiles (split-K only)
   int gn_width;
   float gn_eps;
 };
 
+// Workgroup b runs on XCD b mod 8. When the launch is a multiple of 8, the
+// tile order t = (b mod 8)·(G/8) + b/8 gives each XCD a contiguous range of
+// t (slices fastest, then tile rows, then tile columns), so the slices of a
+// tile share one L2 and so do the tiles that reuse the same W columns.
+__device__ __forceinline__ int xcd_order(int b, int G) {
+  return (G & 7) == 0 ? (b & 7) * (G >> 3) + (b >> 3) : b;
+}
+
+// Split-K exchange. Every slice stores its partial tile with device-coherent
+// 16-byte stores (thread-major, so each wave's stores are contiguous), waits
+// until they are acknowledged and then counts its arrival in the tile's
+// 64-bit counter word (high half: the run's epoch, low half: arrivals in
+// that run) with an atomic compare-and-swap. An arrival that finds another
+// epoch — left by an earlier run, or whatever the workspace held — starts the
+// count at 1 for this run, so the workspace needs no initialisation. The
+// slice that brings the count to ks reads the partials back with
+// device-coherent loads and adds them in slice order (so the sum does not
+// depend on which slice arrives last), resets the count to 0 under the same
+// epoch (a captured graph replaying the launch with the same epoch then
+// starts clean) and returns true. Only the partials and the counter are
+// shared, and both are accessed device-coherently, so no cache-wide
+// write-back or invalidation is needed.
+template <class TL>
+__device__ __forceinline__ bool split_k_gather(const DenseArgs& a, int tile, int ks,
+                                               f32x4 (&acc)[TL::FM][TL::FN], unsigned* flag) {
+  constexpr int NF = TL::FM * TL::FN;
+  constexpr uint32_t SLICE = NF * TL::THREADS * 16;   // bytes of one partial tile
+  const int tid = threadIdx.x;
+  const i32x4 rsrc = make_buffer_rsrc(a.partials + (size_t)tile * a.ks * NF * TL::THREADS,
+                                      static_cast<uint32_t>(a.ks) * SLICE);
+  const uint32_t lane_off = static_cast<uint32_t>(tid) * 16;
+#pragma unroll
+  for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < TL::FN; ++fn)
+      fg_raw_buffer_store_b128(__builtin_bit_cast(i32x4, acc[fm][fn]), rsrc,
+                               ks * SLICE + (fm * TL::FN + fn) * TL::THREADS * 16 + lane_off, 0, FG_CPOL_DEVICE);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (tid == 0) {
+    unsigned long long* word = a.counters + tile;
+    const unsigned long long ep = (unsigned long long)a.epoch << 32;
+    unsigned long long old = __hip_atomic_load(word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), want;
+    while (true) {
+      want = (old & 0xffffffff00000000ull) == ep ? old + 1 : ep | 1ull;
+      if (__hip_atomic_compare_exchange_strong(word, &old, want, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT))
+        break;
+    }
+    *flag = (unsigned)want;
+  }
+  __syncthreads();
+  if (*flag != (unsigned)a.ks) return false;
+  // read back one fragment row (FN loads) at a time: the memory clobber keeps
+  // the compiler from hoisting every load, whose destinations would not fit
+  // beside the accumulators
+#pragma unroll 1
+  for (int k = ks == 0 ? 1 : 0; k < a.ks; ++k) {
+#pragma unroll
+    for (int fm = 0; fm < TL::FM; ++fm) {
+      f32x4 v[TL::FN];
+#pragma unroll
+      for (int fn = 0; fn < TL::FN; ++fn)
+        v[fn] = __builtin_bit_cast(
+            f32x4, fg_raw_buffer_load_b128(rsrc, k * SLICE + (fm * TL::FN + fn) * TL::THREADS * 16 + lane_off, 0,
+                                           FG_CPOL_DEVICE));
+#pragma unroll
+      for (int fn = 0; fn < TL::FN; ++fn) {
+        if (k == 0)
+          acc[fm][fn] = v[fn];
+        else
+          acc[fm][fn] += v[fn];
+      }
+      asm volatile("" ::: "memory");
+    }
+  }
+  if (tid == 0)
+    __hip_atomic_store(a.counters + tile, (unsigned long long)a.epoch << 32, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  return true;
+}
+
 template <class TL, int RED, int OUT>
 __global__ __launch_bounds__(TL::THREADS) void fgemm_kernel(DenseArgs a, EpiArgs ep) {
   __shared__ __attribute__((aligned(16))) char lds[DenseLds<TL>::BYTES];
-  const int tm = blockIdx.x / a.tiles_n, tn = blockIdx.x % a.tiles_n;
+  const int t = xcd_order(blockIdx.x, a.tiles_m * a.tiles_n * a.ks);
+  const int ks = t % a.ks, tile = t / a.ks;
+  const int tm = tile % a.tiles_m, tn = tile / a.tiles_m;
   const int m0 = tm * TL::BM, n0 = tn * TL::BN;
   const int64_t rowbytes = a.K * TL::ESIZE;
-  const int r0 = threadIdx.x >> 3;
+  const int64_t kbeg = ks * a.kslice;
+  const int64_t kbytes = ks == a.ks - 1 ? rowbytes - kbeg : a.kslice;
 
-  RowSet<TL::A_LD> ra;
-  RowSet<TL::B_LD> rb;
-#pragma unroll
-  for (int p = 0; p < TL::A_LD; ++p) {
-    const int m = m0 + r0 + TL::RSTRIDE * p;
-    ra.ptr[p] = a.A + (int64_t)(m < a.M ? m : a.M - 1) * rowbytes;
-  }
-#pragma unroll
-  for (int p = 0; p < TL::B_LD; ++p) {
-    const int n = n0 + r0 + TL::RSTRIDE * p;
-    rb.ptr[p] = a.W + (int64_t)(n < a.N ? n : a.N - 1) * rowbytes;
-  }
+  BufRows<TL::A_LD, TL::RSTRIDE> ra;
+  BufRows<TL::B_LD, TL::RSTRIDE> rb;
+  ra.init(a.A + (int64_t)m0 * rowbytes + kbeg, a.M - m0, TL::BM, rowbytes);
+  rb.init(a.W + (int64_t)n0 * rowbytes + kbeg, a.N - n0, TL::BN, rowbytes);
 
   f32x4 acc[TL::FM][TL::FN];
-  gemm_mainloop<TL>(ra, rb, rowbytes, lds, acc);
+  gemm_mainloop<TL>(ra, rb, kbytes, lds, acc);
+  if (a.ks > 1 && !split_k_gather<TL>(a, tile, ks, acc, reinterpret_cast<unsigned*>(lds))) return;
 
   if (a.bias != nullptr) add_bias<TL>(a.bias, n0, a.N, acc);
   apply_ops<TL>(ep, acc);
@@ -132,10 +224,23 @@ __global__ __launch_bounds__(256) void lse_combine_kernel(const float2* ws, floa
 // kernel table
 
 typedef Tile<In::F32, 64, 128> TileF32;
+typedef Tile<In::BF16, 256, 256, 2, 4> TileHuge;
 typedef Tile<In::BF16, 256, 128, 4, 2> TileBig;
 typedef Tile<In::BF16, 128, 128> TileMid;
 
-enum Cfg : int { CFG_F32 = 0, CFG_BF16_256x128 = 1, CFG_BF16_128x128 = 2 };
+enum Cfg : int { CFG_F32 = 0, CFG_BF16_256x128 = 1, CFG_BF16_128x128 = 2, CFG_BF16_256x256 = 3 };
+
+// Relative MFMA efficiency of the bf16 tiles, measured on 1024..4096-row
+// problems: the larger tile moves fewer bytes from L2 into LDS per FLOP.
+struct TileModel {
+  int cfg, BM, BN;
+  double eff;
+};
+static const TileModel kBf16Tiles[] = {
+    {CFG_BF16_256x256, 256, 256, 1.00},
+    {CFG_BF16_256x128, 256, 128, 0.88},
+    {CFG_BF16_128x128, 128, 128, 0.72},
+};
 
 typedef void (*KernelFn)(DenseArgs, EpiArgs);
 
@@ -172,9 +277,24 @@ struct fg_plan {
   fg_epilogue epi;
   int cfg;
   int BM, BN;
+  int ks;                   // K slices
+  int64_t kslice;           // bytes per row per slice (all but the last)
   int64_t tiles_m, tiles_n;
+  size_t lse_bytes;         // LogSumExp pairs at the start of the workspace
+  size_t cnt_off, part_off; // split-K counters and partial tiles
   size_t ws_bytes;
 };
+
+static size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Split-K run epochs: distinct for every run of the process (0 is skipped),
+// so a counter word left by any other run never matches.
+static std::atomic<unsigned> g_epoch{0};
+static unsigned next_epoch() {
+  unsigned e;
+  do e = g_epoch.fetch_add(1, std::memory_order_relaxed) + 1; while (e == 0);
+  return e;
+}
 
 extern "C" fg_status fgemm_plan(fg_plan** plan, int64_t M, int64_t N, int64_t K, int32_t in_dtype,
                                 int32_t out_dtype, const fg_epilogue* epi) {
@@ -212,6 +332,9 @@ extern "C" fg_status fgemm_plan(fg_plan** plan, int64_t M, int64_t N, int64_t K,
   const int epc = in_dtype == FG_F32 ? 4 : 8;
   if (K % epc != 0)
     return fail(FG_ERR_ALIGNMENT, "fgemm_plan: K=%lld must be a multiple of %d", (long long)K, epc);
+  // tile operands are addressed with 32-bit offsets from the tile's first row
+  if (K * (in_dtype == FG_F32 ? 4 : 2) > (int64_t)(1 << 22))
+    return fail(FG_ERR_UNSUPPORTED, "fgemm_plan: K=%lld exceeds the 4 MiB row limit", (long long)K);
   if (red != FG_RED_LOGSUMEXP_ROW) {
     const int opc = out_dtype == FG_F32 ? 4 : 8;
     if (N % opc != 0)
@@ -237,22 +360,36 @@ extern "C" fg_status fgemm_plan(fg_plan** plan, int64_t M, int64_t N, int64_t K,
   p->in_dt = in_dtype;
   p->out_dt = out_dtype;
   p->epi = *epi;
+  p->ks = 1;
   if (in_dtype == FG_F32) {
     p->cfg = CFG_F32;
     p->BM = TileF32::BM;
     p->BN = TileF32::BN;
   } else {
-    // The 256×128 tile halves the operand traffic per FLOP against 128×128;
-    // use it whenever it still yields at least one tile per compute unit.
-    const int64_t big_tiles = ((M + 255) / 256) * ((N + 127) / 128);
-    if (big_tiles >= 256) {
-      p->cfg = CFG_BF16_256x128;
-      p->BM = 256;
-      p->BN = 128;
-    } else {
-      p->cfg = CFG_BF16_128x128;
-      p->BM = 128;
-      p->BN = 128;
+    // Estimated time of each (tile, K slices) choice: the workgroups one of
+    // the 256 compute units runs × work per workgroup / tile efficiency, with
+    // 3 % per extra slice for the partial-tile exchange. K is split only
+    // when the 256×256 tiles would leave at least three quarters of the
+    // compute units idle: a split concentrates the tail of each tile on one
+    // workgroup and adds the partial-tile exchange, which costs more than it
+    // gains once the tiles already cover much of the chip. Slices stay
+    // powers of two and at least 16 stages of 64 K-values each.
+    double best = 0.0;
+    for (const TileModel& tmod : kBf16Tiles) {
+      const int64_t tiles = ((M + tmod.BM - 1) / tmod.BM) * ((N + tmod.BN - 1) / tmod.BN);
+      for (int ks = 1; ks <= 4; ks *= 2) {
+        if (ks > 1 && (tmod.cfg != CFG_BF16_256x256 || tiles > 64 || K / 64 < 16 * ks)) break;
+        const int64_t per_cu = (tiles * ks + 255) / 256;
+        const double cost = (double)per_cu * tmod.BM * tmod.BN * ((double)K / ks + 64.0) / tmod.eff *
+                            (1.0 + 0.03 * (ks - 1));
+        if (best == 0.0 || cost < best) {
+          best = cost;
+          p->cfg = tmod.cfg;
+          p->BM = tmod.BM;
+          p->BN = tmod.BN;
+          p->ks = ks;
+        }
+      }
     }
   }
   p->tiles_m = (M + p->BM - 1) / p->BM;
@@ -261,7 +398,18 @@ extern "C" fg_status fgemm_plan(fg_plan** plan, int64_t M, int64_t N, int64_t K,
     delete p;
     return fail(FG_ERR_INVALID_ARG, "fgemm_plan: too many tiles");
   }
-  p->ws_bytes = red == FG_RED_LOGSUMEXP_ROW ? (size_t)M * (size_t)p->tiles_n * sizeof(float2) : 0;
+  const int64_t esize = in_dtype == FG_F32 ? 4 : 2;
+  const int64_t stages = K * esize / 128;
+  p->kslice = p->ks > 1 ? (stages / p->ks) * 128 : 0;
+  p->lse_bytes = red == FG_RED_LOGSUMEXP_ROW ? (size_t)M * (size_t)p->tiles_n * sizeof(float2) : 0;
+  p->cnt_off = round256(p->lse_bytes);
+  p->part_off = p->cnt_off;
+  p->ws_bytes = p->lse_bytes;
+  if (p->ks > 1) {
+    const size_t tiles = (size_t)(p->tiles_m * p->tiles_n);
+    p->part_off = round256(p->cnt_off + tiles * sizeof(unsigned long long));
+    p->ws_bytes = p->part_off + tiles * (size_t)p->ks * (size_t)p->BM * (size_t)p->BN * sizeof(float);
+  }
   *plan = p;
   return FG_OK;
 }
@@ -271,14 +419,15 @@ extern "C" size_t fgemm_workspace_bytes(const fg_plan* plan) { return plan ? pla
 extern "C" void fgemm_destroy(fg_plan* plan) { delete plan; }
 
 extern "C" fg_status fgemm_plan_info(const fg_plan* plan, int32_t* tile_m, int32_t* tile_n,
-                                     int64_t* workgroups, int32_t* launches) {
+                                     int64_t* workgroups, int32_t* launches, int32_t* k_slices) {
   clear_error();
   if (plan == nullptr) return fail(FG_ERR_INVALID_ARG, "fgemm_plan_info: plan is NULL");
   if (tile_m) *tile_m = plan->BM;
   if (tile_n) *tile_n = plan->BN;
-  if (workgroups) *workgroups = plan->M == 0 ? 0 : plan->tiles_m * plan->tiles_n;
+  if (workgroups) *workgroups = plan->M == 0 ? 0 : plan->tiles_m * plan->tiles_n * plan->ks;
   if (launches)
     *launches = plan->M == 0 ? 0 : (plan->epi.reduction == FG_RED_LOGSUMEXP_ROW ? 2 : 1);
+  if (k_slices) *k_slices = plan->ks;
   return FG_OK;
 }
 
@@ -314,7 +463,13 @@ extern "C" fg_status fgemm_run(const fg_plan* plan, const void* A, const void* W
   a.M = (int)p.M;
   a.N = (int)p.N;
   a.K = p.K;
+  a.tiles_m = (int)p.tiles_m;
   a.tiles_n = (int)p.tiles_n;
+  a.ks = p.ks;
+  a.kslice = p.kslice;
+  a.counters = p.ks > 1 ? reinterpret_cast<unsigned long long*>(static_cast<char*>(workspace) + p.cnt_off) : nullptr;
+  a.epoch = p.ks > 1 ? next_epoch() : 0;
+  a.partials = p.ks > 1 ? reinterpret_cast<f32x4*>(static_cast<char*>(workspace) + p.part_off) : nullptr;
   a.gn_width = red == FG_RED_GROUPNORM ? (int)(p.N / p.epi.gn_groups) : 0;
   a.gn_eps = p.epi.gn_eps;
   EpiArgs ep;
@@ -329,12 +484,13 @@ extern "C" fg_status fgemm_run(const fg_plan* plan, const void* A, const void* W
   KernelChoice kc{nullptr, 0};
   switch (p.cfg) {
     case CFG_F32: kc = pick_kernel<TileF32>(red, out_k); break;
+    case CFG_BF16_256x256: kc = pick_kernel<TileHuge>(red, out_k); break;
     case CFG_BF16_256x128: kc = pick_kernel<TileBig>(red, out_k); break;
     case CFG_BF16_128x128: kc = pick_kernel<TileMid>(red, out_k); break;
   }
   if (kc.fn == nullptr) return fail(FG_ERR_UNSUPPORTED, "fgemm_run: no kernel for this plan");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const unsigned grid = (unsigned)(p.tiles_m * p.tiles_n);
+  const unsigned grid = (unsigned)(p.tiles_m * p.tiles_n * p.ks);
   hipLaunchKernelGGL(kc.fn, dim3(grid), dim3(kc.threads), 0, s, a, ep);
   if (red == FG_RED_LOGSUMEXP_ROW) {
     const unsigned g2 = (unsigned)((p.M + 3) / 4);

@@ -350,7 +350,7 @@ __device__ __forceinline__ int64_t weight_row(const GroupedArgs& a, int tn, int 
 }
 
 template <class TL, int EPI>
-__global__ __launch_bounds__(TL::THREADS) void grouped_kernel(GroupedArgs a) {
+__global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))) void grouped_kernel(GroupedArgs a) {
   __shared__ __attribute__((aligned(16))) char lds[GroupedLds<TL>::BYTES];
   // Persistent tile loop: workgroup b takes tiles b, b + G, b + 2G, ...
   // (G = gridDim.x, a multiple of 8) up to the tile count read from the
@@ -434,7 +434,7 @@ __global__ __launch_bounds__(TL::THREADS) void grouped_kernel(GroupedArgs a) {
           // clamped SwiGLU: g = min(gate, L), u = clamp(up, −L, L), (u + 1)·g·σ(αg)
           const float g = fminf(acc[fm][fn][i], limit);
           const float u = fminf(fmaxf(acc[fm][fn + 1][i], -limit), limit);
-          v = (u + 1.0f) * (g / (1.0f + expf(-alpha * g)));
+          v = (u + 1.0f) * (g * fast_sigmoid(alpha * g));
           c = ((wn * TL::FN + fn) >> 1) * 16 + (l & 15);
           return true;
         },

@@ -93,13 +93,26 @@ def test_last_error_describes_the_failure():
 
 def test_tile_choice_and_workspace():
     p = L.fgemm_plan(1024, 8192, 8192, "bf16", "bf16", E(has_bias=True))
-    assert p.info() == {"tile_m": 256, "tile_n": 128, "workgroups": 256, "launches": 1}
+    assert p.info() == {"tile_m": 256, "tile_n": 128, "workgroups": 256, "launches": 1, "k_slices": 1}
     assert p.workspace_bytes() == 0
     p = L.fgemm_plan(300, 520, 264, "bf16", "bf16", E())
-    assert p.info()["tile_m"] == 128 and p.info()["workgroups"] == 3 * 5
+    assert p.info()["tile_m"] == 128 and p.info()["workgroups"] == 3 * 5 and p.info()["k_slices"] == 1
+    assert p.workspace_bytes() == 0
     p = L.fgemm_plan(4096, 8192, 4096, "bf16", "f32", E(reduction="lse"))
-    assert p.info()["launches"] == 2
-    assert p.workspace_bytes() == 4096 * 64 * 8
+    assert p.info() == {"tile_m": 256, "tile_n": 256, "workgroups": 512, "launches": 2, "k_slices": 1}
+    assert p.workspace_bytes() == 4096 * 32 * 8
+    # few tiles and a long K: split K over 4 slices (36 tiles → 144 workgroups)
+    p = L.fgemm_plan(1000, 2056, 4104, "bf16", "bf16", E())
+    assert p.info() == {"tile_m": 256, "tile_n": 256, "workgroups": 144, "launches": 1, "k_slices": 4}
+    assert p.workspace_bytes() == 512 + 36 * 4 * 256 * 256 * 4        # counter words, then partials
+    # the shapes the GPU parity tests use for each large-tile configuration
+    for shape, want in (((4000, 4000, 200), (256, 256, 1)), ((2000, 4104, 136), (256, 256, 1)),
+                        ((2048, 4096, 128), (256, 128, 1)), ((512, 1024, 8192), (256, 256, 4))):
+        i = L.fgemm_plan(*shape, "bf16", "bf16", E()).info()
+        assert (i["tile_m"], i["tile_n"], i["k_slices"]) == want, shape
+    with pytest.raises(L.FgError) as ei:
+        L.fgemm_plan(64, 64, 1 << 22, "bf16", "bf16", E())            # 8 MiB rows
+    assert ei.value.status == L.FG_ERR_UNSUPPORTED
     p = L.fgemm_plan(0, 8192, 4096, "bf16", "bf16", E())
     assert p.info()["workgroups"] == 0 and p.info()["launches"] == 0
     p = L.fgemm_plan(128, 256, 256, "f32", "f32", E())

@@ -3,9 +3,10 @@
 Every case runs the HIP kernels through the C ABI on seeded inputs and
 compares element by element with ``oracle.ref_fgemm`` under the RMS-floored
 relative error: ≤ 1e-4 for fp32 inputs, ≤ 1e-2 for bf16 inputs. Sizes span
-several tiles with ragged M, N and K tails and cover both bf16 tile
-configurations; the full-size workloads are checked on sampled rows (each
-output row depends only on its own input row)."""
+several tiles with ragged M, N and K tails and cover every bf16 tile
+configuration (128×128, 256×128, 256×256, and 256×256 with K split over
+slices) with each tail; the full-size workloads are checked on sampled rows
+(each output row depends only on its own input row)."""
 
 import numpy as np
 import pytest
@@ -58,13 +59,20 @@ SMALL = [
     C1,                                               # the fp32 workload at full size
     C1.scaled(M=77, N=200, K=36, name="f32_ragged"),  # K tail (36 % 32), ragged M, N
     C2.scaled(M=300, N=520, K=264),                   # 128×128 tiles, ragged, K tail
-    C2.scaled(M=2000, N=4104, K=136),                 # 256×128 tiles (≥ 256 of them), ragged
+    C2.scaled(M=2000, N=4104, K=136),                 # 256×256 tiles, ragged, K tail
+    C2.scaled(M=4000, N=4000, K=200),                 # 256×256 tiles filling the chip, ragged
+    C2.scaled(M=1000, N=2056, K=4104),                # split-K over 4 slices, ragged, K tail
+    C2.scaled(M=512, N=1024, K=8192),                 # split-K over 4 slices, 8 tiles
     C3.scaled(M=300, N=1000, K=264),                  # LSE across 8 N tiles, ragged N
     C3.scaled(M=70, N=100, K=64),                     # LSE inside one partial tile
     C3.scaled(M=2048, N=4096, K=128),                 # LSE with 256×128 tiles
+    C3.scaled(M=4000, N=4000, K=200),                 # LSE with 256×256 tiles, ragged N
+    C3.scaled(M=1000, N=2056, K=4104),                # LSE after a split-K gather
     C4.scaled(M=300, N=512, K=264),                   # GroupNorm, 4 groups of 128
     FgemmSpec("gn64_ragged", 133, 320, 72, "bf16", 1 / 64, (("silu",),), "groupnorm", 5, 1e-5),
     C4.scaled(M=2048, N=4096, K=128),                 # GroupNorm with 256×128 tiles
+    C4.scaled(M=4000, N=4096, K=200),                 # GroupNorm with 256×256 tiles
+    C4.scaled(M=1000, N=2048, K=4104),                # GroupNorm after a split-K gather
     FgemmSpec("f32_gn_lse_chain", 96, 256, 64, "f32", 0.2, (("gelu_tanh",), ("scale", 1.5)), "lse"),
     FgemmSpec("f32_gn", 96, 256, 64, "f32", 0.2, (("silu",),), "groupnorm", 2, 1e-5),
     FgemmSpec("bf16_all_ops", 130, 264, 200, "bf16", 0.1,
@@ -150,3 +158,27 @@ def test_run_errors_on_device():
         L.fgemm_run(plan, x.data_ptr(), W.data_ptr(), None, None, None, out.data_ptr(), None, 0,
                     torch.cuda.current_stream().cuda_stream)
     assert ei.value.status == L.FG_ERR_WORKSPACE
+
+
+def test_split_k_ignores_workspace_contents_and_repeats_bit_identically():
+    """The split-K arrival counters work from any initial value: a workspace
+    full of random bytes gives the same, correct result, run after run."""
+    require_gpu()
+    spec = C2.scaled(M=1000, N=2056, K=4104)
+    plan = api.get_plan(spec.M, spec.N, spec.K, "bf16", "bf16", True, spec.ops)
+    assert plan.info()["k_slices"] == 4
+    inp = make_fgemm_inputs(spec, 5)
+    (x, W, b, _, _), (x64, W64) = _device_inputs(spec, inp)
+    ws = torch.randint(0, 256, (plan.workspace_bytes(),), dtype=torch.uint8, device="cuda")
+    outs = []
+    for _ in range(3):
+        outs.append(api.linear_epilogue(x, W, b, spec.ops, workspace=ws))
+        ws[:512].random_(0, 256)              # scramble the counter words between runs
+    torch.cuda.synchronize()
+    for o in outs[1:]:
+        assert torch.equal(o.view(torch.int16), outs[0].view(torch.int16))
+    rows = np.array([0, 1, 255, 256, 511, 767, 998, 999])
+    ref = ref_fgemm(x64[rows], W64, inp["b"].astype(np.float64), spec.ops)
+    rep = compare(host64(outs[0])[rows], ref, "bf16")
+    log(f"    {rep}")
+    assert rep.ok, rep
