@@ -280,6 +280,44 @@ def bench_moe(args, torch, np):
                      f"{spec.w_dtype} weights, clamped SwiGLU",
          "T": spec.T, "H": spec.H, "I": spec.I, "E": spec.E, "top_k": spec.k}, roof)
     result["hbm_gbs"] = round(gbs, 1)
+
+    if not args.no_unfused and spec.w_dtype == "bf16":
+        # The eager PyTorch sequence: top-k and softmax, a stable argsort of the
+        # slots, the expert sizes brought to the host for the per-expert loop,
+        # a gather of token rows, per expert a vendor GEMM, the clamped SwiGLU
+        # as separate elementwise kernels and a second vendor GEMM, then the
+        # routing-weight multiply, a scatter back to slot order and the sum
+        # over the k slots.
+        import torch.nn.functional as F  # noqa: F401
+        k, E, I = spec.k, spec.E, spec.I
+
+        def unfused():
+            topv, topi = torch.topk(lg, k, dim=1)
+            wts = torch.softmax(topv, dim=1).flatten()
+            flat = topi.flatten()
+            order = torch.argsort(flat, stable=True)
+            offs = [0] + torch.bincount(flat, minlength=E).cumsum(0).tolist()
+            xs = x[order // k]
+            ys = torch.empty(x.shape[0] * k, spec.H, dtype=torch.bfloat16, device=dev)
+            for e in range(E):
+                a, b_ = offs[e], offs[e + 1]
+                if a == b_:
+                    continue
+                gu = torch.mm(xs[a:b_], wgu[e].t())
+                gate = torch.clamp(gu[:, :I], max=spec.limit)
+                up = torch.clamp(gu[:, I:], -spec.limit, spec.limit)
+                h = (up + 1) * gate * torch.sigmoid(spec.alpha * gate)
+                ys[order[a:b_]] = torch.mm(h, wd[e].t())
+            ys = ys * wts[:, None].to(torch.bfloat16)
+            return ys.view(-1, k, spec.H).float().sum(1).to(torch.bfloat16)
+
+        ms_u = time_steps(unfused, args.steps, args.warmup, torch)
+        result["unfused"] = {"ms": round(ms_u, 5), "tflops": round(flops / (ms_u * 1e-3) / 1e12, 2),
+                             "hbm_gbs": round(nbytes / (ms_u * 1e-3) / 1e9, 1),
+                             "sequence": "eager torch: topk, softmax, stable argsort, per-expert "
+                                         "torch.mm + elementwise clamped SwiGLU + torch.mm, weighted "
+                                         "scatter, slot sum"}
+        result["speedup_vs_unfused"] = round(ms_u / ms, 3)
     return result
 
 

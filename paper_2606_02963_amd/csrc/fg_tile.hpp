@@ -331,10 +331,12 @@ __device__ __forceinline__ void gemm_mainloop(const LA& ra, const LB& rb,
     wait_vmem();
   }
   __syncthreads();
-  if constexpr (SUB == 1) {
-    // e4m3: one substep per stage and 32-byte fragments; a second fragment
-    // set would not fit beside two resident workgroups, so each wave reads
-    // and multiplies in turn and the other workgroup's waves fill the gaps.
+  if constexpr (SUB == 1 && TL::FM * TL::FN > 8) {
+    // large e4m3 tiles: one substep per stage and 32-byte fragments; a
+    // second fragment set would not fit beside two resident workgroups, so
+    // each wave reads and multiplies in turn and the other workgroup's waves
+    // fill the gaps. (Small e4m3 tiles take the pipelined loop below, with
+    // one stage per substep.)
     for (int64_t kt = 0; kt < KT; ++kt) {
       read_frag<TL>(lds + (kt & 1) * TL::STAGE_BYTES, wm, wn, 0, F0);
       mma_frag<TL>(F0, acc);

@@ -107,23 +107,25 @@ __device__ __forceinline__ void place_slots(const int32_t* topk_idx, int s_begin
 
 // Exclusive prefix of the per-expert totals `tot` (in place) and of their
 // m-tile counts, by wave 0: lane l owns experts 4l .. 4l + 3 (E ≤ 256), then a
-// wave-wide scan of the lane sums. Workgroup 0 also publishes offsets and
-// the m-tile prefix.
+// scan of the lane sums over the ceil(E/4) lanes that hold experts.
+// Workgroup 0 also publishes offsets and the m-tile prefix. BM is a power of
+// two.
 __device__ __forceinline__ void publish_offsets(int* tot, int E, int BM, int32_t* offsets, int32_t* tile_off) {
   if (threadIdx.x < 64) {
     const int lane = threadIdx.x;
+    const int bm_shift = __builtin_ctz((unsigned)BM);
+    const int nlanes = (E + 3) >> 2;
     int c[4], tc[4], s = 0, ts = 0;
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
       const int e = 4 * lane + q;
       c[q] = e < E ? tot[e] : 0;
-      tc[q] = (c[q] + BM - 1) / BM;
+      tc[q] = (c[q] + BM - 1) >> bm_shift;
       s += c[q];
       ts += tc[q];
     }
     int incl = s, tincl = ts;
-#pragma unroll
-    for (int d = 1; d < 64; d <<= 1) {
+    for (int d = 1; d < nlanes; d <<= 1) {
       const int y = __shfl_up(incl, d, 64), ty = __shfl_up(tincl, d, 64);
       if (lane >= d) {
         incl += y;
@@ -144,12 +146,33 @@ __device__ __forceinline__ void publish_offsets(int* tot, int E, int BM, int32_t
       acc += c[q];
       tacc += tc[q];
     }
-    if (blockIdx.x == 0 && lane == 63) {
+    if (blockIdx.x == 0 && lane == nlanes - 1) {
       offsets[E] = incl;
       tile_off[E] = tincl;
     }
   }
   __syncthreads();
+}
+
+// Largest of a 64-bit key over the 4 lanes of a quad (DPP quad permutes
+// lane ^ 1 and lane ^ 2 on both halves).
+__device__ __forceinline__ uint64_t quad_max_u64(uint64_t m) {
+  uint32_t lo = (uint32_t)m, hi = (uint32_t)(m >> 32);
+  uint64_t o;
+  lo = (uint32_t)m;
+  o = ((uint64_t)(uint32_t)__builtin_amdgcn_update_dpp(0, (int)hi, 0xB1, 0xF, 0xF, false) << 32) |
+      (uint32_t)__builtin_amdgcn_update_dpp(0, (int)lo, 0xB1, 0xF, 0xF, false);
+  m = o > m ? o : m;
+  lo = (uint32_t)m;
+  hi = (uint32_t)(m >> 32);
+  o = ((uint64_t)(uint32_t)__builtin_amdgcn_update_dpp(0, (int)hi, 0x4E, 0xF, 0xF, false) << 32) |
+      (uint32_t)__builtin_amdgcn_update_dpp(0, (int)lo, 0x4E, 0xF, 0xF, false);
+  return o > m ? o : m;
+}
+__device__ __forceinline__ float quad_sum(float v) {
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0xB1, 0xF, 0xF, false));
+  v += __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x4E, 0xF, 0xF, false));
+  return v;
 }
 
 template <bool FUSED_PLACE>
@@ -161,6 +184,7 @@ __global__ __launch_bounds__(64 * ROUTE_WAVES) void moe_route_kernel(const float
   // row pitch E + 1 floats: thread t reading its row's logit e hits bank (t·(E+1) + e) mod 64
   __shared__ float lg[ROUTE_TOKENS * (EMAX + 1)];
   __shared__ int hist[EMAX];
+  __shared__ int32_t chosen[FUSED_PLACE ? ROUTE_TOKENS * KMAX : 1];   // the block's slots, for placement
   __shared__ uint32_t masks[FUSED_PLACE ? EMAX * PLACE_WORDS : 1];
   const int t0 = blockIdx.x * ROUTE_TOKENS;
   const int nt = T - t0 < ROUTE_TOKENS ? T - t0 : ROUTE_TOKENS;
@@ -193,28 +217,39 @@ __global__ __launch_bounds__(64 * ROUTE_WAVES) void moe_route_kernel(const float
   int sel_i = -1;           // lane q of the quad keeps selection q (and q + 4)
   int sel_i2 = -1;
   float sel_v = -INFINITY, sel_v2 = -INFINITY, top = -INFINITY;
-  for (int j = 0; j < k; ++j) {
-    uint64_t part[4] = {0, 0, 0, 0};
-    for (int e0 = sub; e0 < E; e0 += 16) {
+  // E ≤ 32: the lane's (at most 8) keys stay in registers for all k passes
+  constexpr int KPL = 8;
+  uint64_t keys[KPL];
+  const bool in_regs = E <= 4 * KPL;
+  if (in_regs) {
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int e = e0 + 4 * u;
-        if (e < E) {
-          const uint64_t key = logit_key(row[e], e);
-          part[u] = (key < win && key > part[u]) ? key : part[u];
+    for (int u = 0; u < KPL; ++u) {
+      const int e = sub + 4 * u;
+      keys[u] = e < E ? logit_key(row[e], e) : 0ull;
+    }
+  }
+  for (int j = 0; j < k; ++j) {
+    uint64_t m = 0;
+    if (in_regs) {
+#pragma unroll
+      for (int u = 0; u < KPL; ++u) m = (keys[u] < win && keys[u] > m) ? keys[u] : m;
+    } else {
+      uint64_t part[4] = {0, 0, 0, 0};
+      for (int e0 = sub; e0 < E; e0 += 16) {
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const int e = e0 + 4 * u;
+          if (e < E) {
+            const uint64_t key = logit_key(row[e], e);
+            part[u] = (key < win && key > part[u]) ? key : part[u];
+          }
         }
       }
+      m = part[0] > part[1] ? part[0] : part[1];
+      const uint64_t m2 = part[2] > part[3] ? part[2] : part[3];
+      m = m > m2 ? m : m2;
     }
-    uint64_t m = part[0] > part[1] ? part[0] : part[1];
-    const uint64_t m2 = part[2] > part[3] ? part[2] : part[3];
-    m = m > m2 ? m : m2;
-#pragma unroll
-    for (int d = 1; d <= 2; d <<= 1) {
-      const uint32_t lo = __shfl_xor((uint32_t)m, d, 64), hi = __shfl_xor((uint32_t)(m >> 32), d, 64);
-      const uint64_t o = ((uint64_t)hi << 32) | lo;
-      m = o > m ? o : m;
-    }
-    win = m;
+    win = quad_max_u64(m);
     const int e = EMAX - 1 - (int)(win & 0xffffffffu);
     const float v = key_value(win);
     if (j == 0) top = v;
@@ -229,28 +264,28 @@ __global__ __launch_bounds__(64 * ROUTE_WAVES) void moe_route_kernel(const float
   }
   const float ex = sub < k ? expf(sel_v - top) : 0.0f;
   const float ex2 = sub + 4 < k ? expf(sel_v2 - top) : 0.0f;
-  float sum = ex + ex2;
-#pragma unroll
-  for (int d = 1; d <= 2; d <<= 1) sum += __shfl_xor(sum, d, 64);
+  const float sum = quad_sum(ex + ex2);
   if (active) {
     const int t = t0 + tt;
     if (sub < k) {
       topk_idx[(int64_t)t * k + sub] = sel_i;
       topk_w[(int64_t)t * k + sub] = ex / sum;
       atomicAdd(&hist[sel_i], 1);
+      if constexpr (FUSED_PLACE) chosen[tt * k + sub] = sel_i;
     }
     if (sub + 4 < k) {
       topk_idx[(int64_t)t * k + sub + 4] = sel_i2;
       topk_w[(int64_t)t * k + sub + 4] = ex2 / sum;
       atomicAdd(&hist[sel_i2], 1);
+      if constexpr (FUSED_PLACE) chosen[tt * k + sub + 4] = sel_i2;
     }
   }
   __syncthreads();
   if constexpr (FUSED_PLACE) {
-    // the only workgroup: its histogram is the total; topk_idx written above
-    // by this workgroup is visible after the barrier
+    // the only workgroup: its histogram is the total, and its slots' experts
+    // are in LDS (no round trip through the topk_idx stores)
     publish_offsets(hist, E, BM, offsets, tile_off);
-    place_slots<64 * ROUTE_WAVES>(topk_idx, 0, T * k, E, hist, masks, perm);
+    place_slots<64 * ROUTE_WAVES>(chosen, 0, T * k, E, hist, masks, perm);
   } else {
     for (int e = threadIdx.x; e < E; e += 64 * ROUTE_WAVES) block_counts[(int64_t)blockIdx.x * E + e] = hist[e];
   }
