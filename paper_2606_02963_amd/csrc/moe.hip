@@ -371,11 +371,14 @@ struct GroupedLds {
 // block f (ρ/16) is gate (f even) or up (f odd) of output columns
 // (f/2)·16 .. +15, so a lane's accumulators for fragment pairs (2q, 2q+1)
 // hold matching gate and up values.
+// Columns of h past I (the ragged last n-tile) read the last column's rows;
+// their results are never stored.
 template <class TL, int EPI>
 __device__ __forceinline__ int64_t weight_row(const GroupedArgs& a, int tn, int rho) {
   if constexpr (EPI == EPI_GATEUP) {
     const int f = rho >> 4;
-    const int64_t hc = (int64_t)tn * (TL::BN / 2) + (f >> 1) * 16 + (rho & 15);
+    int64_t hc = (int64_t)tn * (TL::BN / 2) + (f >> 1) * 16 + (rho & 15);
+    hc = hc < a.I ? hc : a.I - 1;
     const int up = f & 1;
     return a.interleaved ? 2 * hc + up : up * a.I + hc;
   } else {
@@ -477,7 +480,7 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
           const int row = r0 + r;
           return row < seg1 ? out + ((int64_t)row * ldo + c0) * 2 : nullptr;
         },
-        TL::BN / 2);
+        (int)(a.I - c0 < TL::BN / 2 ? a.I - c0 : TL::BN / 2));
   } else {
     char* out = a.out;
     const int64_t ldo = a.ldo;
@@ -633,7 +636,7 @@ static int resident_workgroups() {
 
 template <class TL, int EPI>
 static void launch_grouped(GroupedArgs a, int64_t S, hipStream_t s) {
-  a.tiles_n = EPI == EPI_GATEUP ? (int)(a.I / (TL::BN / 2)) : (int)((a.Nw + TL::BN - 1) / TL::BN);
+  a.tiles_n = EPI == EPI_GATEUP ? (int)((a.I + TL::BN / 2 - 1) / (TL::BN / 2)) : (int)((a.Nw + TL::BN - 1) / TL::BN);
   a.tiles_n_grid = (a.tiles_n + 7) / 8 * 8;
   // the m-tile count is known only on the device; its upper bound is
   // Σ_e ceil(n_e / BM) ≤ (S + E·(BM − 1)) / BM
