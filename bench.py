@@ -29,6 +29,7 @@ PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published
 PEAK_HBM_GBS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = ["fg_tile.hpp", "fg_epilogue.hpp", "fgemm.hip"]
+MOE_KERNEL_SOURCES = ["fg_tile.hpp", "fg_quant.hpp", "moe.hip", "quant.hip"]
 
 
 def parse():
@@ -52,15 +53,15 @@ def parse():
     return ap.parse_args()
 
 
-def kernel_source_hash():
+def kernel_source_hash(sources=KERNEL_SOURCES):
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in sources:
         with open(os.path.join(ROOT, "paper_2606_02963_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
 
 
-def measured_traffic(name):
+def measured_traffic(name, sources=KERNEL_SOURCES):
     """HBM bytes per launch from committed rocprofv3 --pmc summaries
     (FETCH_SIZE + WRITE_SIZE, copy-kernel calibrated) if they were taken on
     the current kernel sources; None otherwise."""
@@ -69,7 +70,7 @@ def measured_traffic(name):
         return None
     with open(path) as fh:
         d = json.load(fh)
-    if d.get("kernel_source_hash") != kernel_source_hash():
+    if d.get("kernel_source_hash") != kernel_source_hash(sources):
         return None
     return d.get("hbm_bytes_per_launch")
 
@@ -271,7 +272,8 @@ def bench_moe(args, torch, np):
              "frac": round(gbs / PEAK_HBM_GBS, 4)} if decode else
             {"bound": "mfma", "achieved": round(tflops, 2), "peak": peak_c, "unit": "TFLOP/s",
              "frac": round(tflops / peak_c, 4)})
-    roof.update({"traffic": measured_traffic(f"moe_{spec.name}"), "scope": "whole step (all launches)",
+    roof.update({"traffic": measured_traffic(spec.name, MOE_KERNEL_SOURCES),
+                 "scope": "whole step (all launches)",
                  "algorithmic_flops": flops, "algorithmic_bytes": nbytes, "active_experts": active})
     result = base_result(
         args, tflops, ms, "e4m3" if spec.w_dtype == "e4m3" else "bf16",
