@@ -390,6 +390,24 @@ __device__ __forceinline__ int64_t weight_row(const GroupedArgs& a, int tn, int 
 template <class TL, int EPI>
 __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))) void grouped_kernel(GroupedArgs a) {
   __shared__ __attribute__((aligned(16))) char lds[GroupedLds<TL>::BYTES];
+  // The m-tile prefix and the expert offsets, read once per workgroup into
+  // registers (entry i in lane i mod 64, register i / 64; E ≤ 256): the
+  // expert of an m-tile is then the number of experts whose tiles end at or
+  // before it (a ballot), and its offsets come from lane shuffles, instead
+  // of a chain of dependent global loads per tile.
+  const int lane = threadIdx.x & 63;
+  int toff_end[4], off_beg[4];   // tile_off[i + 1] (INT_MAX past E), offsets[i] (i ≤ E)
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int i = lane + 64 * q;
+    toff_end[q] = i < a.E ? a.tile_off[i + 1] : 0x7fffffff;
+    off_beg[q] = i <= a.E ? a.offsets[i] : 0;
+  }
+  auto pick = [&](const int (&v)[4], int i) {   // v[i / 64] of lane i mod 64 (i wave-uniform)
+    const int q = i >> 6;
+    const int x = q == 0 ? v[0] : q == 1 ? v[1] : q == 2 ? v[2] : v[3];
+    return __shfl(x, i & 63, 64);
+  };
   // Persistent tile loop: workgroup b takes tiles b, b + G, b + 2G, ...
   // (G = gridDim.x, a multiple of 8) up to the tile count read from the
   // device-side m-tile prefix, which every workgroup reaches. Tile t is
@@ -397,20 +415,16 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
   // tiles_n_grid and G multiples of 8 and workgroups dealt to the 8 XCDs
   // round-robin, every m-tile of a given n-tile runs on the same XCD, so the
   // weight tile is fetched into one L2 and reused there.
-  const int ntiles = a.tile_off[a.E] * a.tiles_n_grid;
+  const int ntiles = pick(toff_end, a.E - 1) * a.tiles_n_grid;
   for (int t = blockIdx.x; t < ntiles; t += gridDim.x) {
   const int tn = t % a.tiles_n_grid;
   const int mt = t / a.tiles_n_grid;
   if (tn >= a.tiles_n) continue;
-  int lo = 0, hi = a.E;        // tile_off[lo] ≤ mt < tile_off[hi]
-  while (hi - lo > 1) {
-    const int mid = (lo + hi) >> 1;
-    if (a.tile_off[mid] <= mt) lo = mid;
-    else hi = mid;
-  }
-  const int e = lo;
-  const int seg0 = a.offsets[e], seg1 = a.offsets[e + 1];
-  const int r0 = seg0 + (mt - a.tile_off[e]) * TL::BM;
+  int e = 0;
+#pragma unroll
+  for (int q = 0; q < 4; ++q) e += __popcll(__ballot(toff_end[q] <= mt));
+  const int seg0 = pick(off_beg, e), seg1 = pick(off_beg, e + 1);
+  const int r0 = seg0 + (mt - (e == 0 ? 0 : pick(toff_end, e - 1))) * TL::BM;
   const int64_t rowbytes = a.K * TL::ESIZE;
   const int tr = threadIdx.x >> 3;
 
@@ -427,12 +441,10 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
 #pragma unroll
   for (int p = 0; p < TL::B_LD; ++p) rb.ptr[p] = We + weight_row<TL, EPI>(a, tn, tr + TL::RSTRIDE * p) * rowbytes;
 
-  f32x4 acc[TL::FM][TL::FN];
-  gemm_mainloop<TL>(ra, rb, rowbytes, lds, acc);
-
-  const int l = threadIdx.x & 63, wave = threadIdx.x >> 6, wn = wave % TL::WN;
-  // per accumulator row: the scale of its activation row (e4m3) and, for the
-  // down GEMM, the routing weight of its slot
+  // Epilogue factors, loaded before the K loop so that their dependent
+  // loads (slot → token → scale) complete behind it: per accumulator row the
+  // scale of its activation row (e4m3) and, for the down GEMM, the routing
+  // weight of its slot; per column the weight-row scale (e4m3).
   float rs[TL::FM][4];
 #pragma unroll
   for (int fm = 0; fm < TL::FM; ++fm)
@@ -440,11 +452,11 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
     for (int i = 0; i < 4; ++i) {
       int r = r0 + acc_row<TL>(fm, i);
       r = r < seg1 ? r : seg0;
-      float s = 1.0f;
+      float sc = 1.0f;
       if constexpr (TL::IN == In::E4M3)
-        s = EPI == EPI_GATEUP ? a.a_scale[a.perm[r] / a.k] : a.a_scale[r];
-      if constexpr (EPI == EPI_DOWN) s *= a.topk_w[a.perm[r]];
-      rs[fm][i] = s;
+        sc = EPI == EPI_GATEUP ? a.a_scale[a.perm[r] / a.k] : a.a_scale[r];
+      if constexpr (EPI == EPI_DOWN) sc *= a.topk_w[a.perm[r]];
+      rs[fm][i] = sc;
     }
   float ws[TL::FN];
 #pragma unroll
@@ -453,6 +465,11 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
     if constexpr (TL::IN == In::E4M3)
       ws[fn] = a.w_scale[(int64_t)e * a.Nw + weight_row<TL, EPI>(a, tn, acc_col<TL>(fn))];
   }
+
+  f32x4 acc[TL::FM][TL::FN];
+  gemm_mainloop<TL>(ra, rb, rowbytes, lds, acc);
+
+  const int l = threadIdx.x & 63, wave = threadIdx.x >> 6, wn = wave % TL::WN;
 #pragma unroll
   for (int fm = 0; fm < TL::FM; ++fm)
 #pragma unroll
