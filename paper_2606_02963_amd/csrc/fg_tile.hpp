@@ -5,9 +5,12 @@
 // (8 chunks of 16 B): 32 fp32, 64 bf16 or 128 e4m3 values. Stages are staged
 // HBM → VGPR → LDS with 128-bit loads and stores and double-buffered in LDS,
 // so the global loads of stage k+1 are in flight while stage k feeds the
-// matrix cores. Inside LDS each row's chunk c is stored at chunk c ^ (row & 7)
-// so that both the row-wise writes and the column-of-rows fragment reads hit
-// eight distinct 16-byte bank groups.
+// matrix cores. Inside LDS each row's chunk c is stored at chunk
+// c ^ (row & 7) ^ ((row >> 3) & 1): a fragment read (16 consecutive rows, one
+// chunk) then touches sixteen distinct 16-byte bank groups of the 64-bank
+// LDS (rows alternate between its two 128-byte halves; the eight rows of one
+// parity land on eight distinct chunks), and any eight consecutive rows also
+// stay distinct, while the row-wise writes remain contiguous.
 //
 // Fragments use the 16 × 16 MFMA shapes of gfx950 (wave64):
 //   bf16  v_mfma_f32_16x16x32_bf16          (two per stage per fragment pair)
@@ -60,7 +63,7 @@ struct Tile {
 };
 
 __device__ __forceinline__ int lds_off(int row, int chunk) {
-  return row * 128 + ((chunk ^ (row & 7)) << 4);
+  return row * 128 + ((chunk ^ (row & 7) ^ ((row >> 3) & 1)) << 4);
 }
 
 // Row sources for the stage loads. Thread t owns tile rows
@@ -71,7 +74,8 @@ __device__ __forceinline__ int lds_off(int row, int chunk) {
 // The direct loads write lane i's 16 bytes at LDS offset 16·i of a
 // wave-uniform 1 KiB block, i.e. block b = wave + NWAVES·p holds tile rows
 // 8b .. 8b + 7 with physical chunk i & 7; the lane therefore fetches logical
-// chunk (i & 7) ^ (i >> 3), the inverse of the LDS swizzle.
+// chunk (i & 7) ^ (i >> 3) ^ (b & 1), the inverse of the LDS swizzle. NWAVES
+// is even, so b & 1 = wave & 1 for every p.
 
 // Gathered rows (MoE token rows through the permutation): one pointer per
 // owned row. Rows past the matrix edge point at any valid row: their LDS copy
@@ -82,8 +86,9 @@ struct RowSet {
 
   template <int NWAVES>
   __device__ __forceinline__ void stage(int64_t kbyte, char* sbase) const {
+    static_assert(NWAVES % 2 == 0, "the fetched chunk assumes an even wave count");
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int c = (lane & 7) ^ (lane >> 3);
+    const int c = (lane & 7) ^ (lane >> 3) ^ (wave & 1);
 #pragma unroll
     for (int p = 0; p < NLD; ++p) {
       const char* src = ptr[p] + kbyte + c * 16;
@@ -146,12 +151,14 @@ struct BufRows {
     rsrc = make_buffer_rsrc(base, static_cast<uint32_t>(rows * row_stride));
     stride = static_cast<uint32_t>(row_stride);
     pstride = static_cast<uint32_t>(RSTRIDE * row_stride);
-    const int lane = threadIdx.x & 63;
-    voff = static_cast<uint32_t>(threadIdx.x >> 3) * stride + static_cast<uint32_t>(((lane & 7) ^ (lane >> 3)) * 16);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    voff = static_cast<uint32_t>(threadIdx.x >> 3) * stride +
+           static_cast<uint32_t>(((lane & 7) ^ (lane >> 3) ^ (wave & 1)) * 16);
   }
 
   template <int NWAVES>
   __device__ __forceinline__ void stage(int64_t kbyte, char* sbase) const {
+    static_assert(NWAVES % 2 == 0, "the fetched chunk assumes an even wave count");
     const int wave = threadIdx.x >> 6;
 #pragma unroll
     for (int p = 0; p < NLD; ++p) {
