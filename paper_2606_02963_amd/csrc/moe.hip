@@ -3,6 +3,7 @@
 // Launch sequence on the caller's stream, with no host synchronisation (the
 // per-expert counts never leave the device):
 //   [e4m3 only] quantise tokens per row          quantize_rows_kernel
+//     (with one routing block: inside the routing launch)
 //   route: top-k + softmax per token, and the    moe_route_kernel
 //     expert histogram of each block of tokens
 //   offsets, stable permutation, m-tile prefix   moe_place_kernel
@@ -180,7 +181,14 @@ __global__ __launch_bounds__(64 * ROUTE_WAVES) void moe_route_kernel(const float
                                                                      int32_t* topk_idx, float* topk_w,
                                                                      int32_t* block_counts, int BM,
                                                                      int32_t* offsets, int32_t* tile_off,
-                                                                     int32_t* perm) {
+                                                                     int32_t* perm, const uint16_t* xq_src,
+                                                                     int64_t H, uint8_t* xq, float* sx) {
+  // Single-block routing may share its launch with the e4m3 quantisation of
+  // the tokens (independent work): blocks 1, 2, ... take four token rows each.
+  if (FUSED_PLACE && blockIdx.x > 0) {
+    quantize_row_wave(xq_src, T, H, xq, sx, (int64_t)(blockIdx.x - 1) * 4 + (threadIdx.x >> 6));
+    return;
+  }
   // row pitch E + 1 floats: thread t reading its row's logit e hits bank (t·(E+1) + e) mod 64
   __shared__ float lg[ROUTE_TOKENS * (EMAX + 1)];
   __shared__ int hist[EMAX];
@@ -720,19 +728,25 @@ extern "C" fg_status moe_grouped_ffn(const moe_desc* d, const void* tokens, cons
   }
   const char* a_tokens = static_cast<const char*>(tokens);
   float* sx = reinterpret_cast<float*>(ws + L.sx);
+  uint8_t* xq = f8 ? reinterpret_cast<uint8_t*>(ws + L.xq) : nullptr;
+  const uint16_t* tok16 = static_cast<const uint16_t*>(tokens);
   if (f8) {
-    hipLaunchKernelGGL(quantize_rows_kernel, dim3((unsigned)((d->T + 3) / 4)), dim3(256), 0, s,
-                       static_cast<const uint16_t*>(tokens), d->T, d->H, reinterpret_cast<uint8_t*>(ws + L.xq), sx);
     a_tokens = ws + L.xq;
+    if (L.nblocks > 1)
+      hipLaunchKernelGGL(quantize_rows_kernel, dim3((unsigned)((d->T + 3) / 4)), dim3(256), 0, s, tok16, d->T,
+                         d->H, xq, sx);
   }
   int32_t* counts = reinterpret_cast<int32_t*>(ws + L.counts);
   if (L.nblocks == 1) {
-    hipLaunchKernelGGL(moe_route_kernel<true>, dim3(1), dim3(64 * ROUTE_WAVES), 0, s, router_logits, T, d->E,
-                       d->top_k, topk_idx, topk_w, counts, L.BM, expert_offsets, tile_off, perm);
+    // one routing block; with e4m3 the token quantisation rides in the same launch
+    const unsigned qblocks = f8 ? (unsigned)((d->T + 3) / 4) : 0u;
+    hipLaunchKernelGGL(moe_route_kernel<true>, dim3(1 + qblocks), dim3(64 * ROUTE_WAVES), 0, s, router_logits, T,
+                       d->E, d->top_k, topk_idx, topk_w, counts, L.BM, expert_offsets, tile_off, perm, tok16, d->H,
+                       xq, sx);
   } else {
     hipLaunchKernelGGL(moe_route_kernel<false>, dim3((unsigned)L.nblocks), dim3(64 * ROUTE_WAVES), 0, s,
                        router_logits, T, d->E, d->top_k, topk_idx, topk_w, counts, L.BM, expert_offsets, tile_off,
-                       perm);
+                       perm, tok16, d->H, xq, sx);
     hipLaunchKernelGGL(moe_place_kernel, dim3((unsigned)L.nblocks), dim3(64 * PLACE_WAVES), 0, s, topk_idx, counts,
                        (int)S, d->E, d->top_k, L.nblocks, L.BM, expert_offsets, tile_off, perm);
   }
