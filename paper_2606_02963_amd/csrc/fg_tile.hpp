@@ -98,17 +98,23 @@ struct RowSet {
     }
   }
 
+  // Every load is issued before the first LDS write (global address space,
+  // so the compiler need not order them after the writes): one memory round
+  // trip. Chunks past kbytes load the row's first chunk and are replaced by
+  // zeros.
   template <int RSTRIDE>
   __device__ __forceinline__ void tail(int64_t kbyte, int64_t kbytes, char* sbase) const {
+    typedef const __attribute__((address_space(1))) i32x4 GlobalChunk;
     const int c = threadIdx.x & 7;
     const int r0 = threadIdx.x >> 3;
     const int64_t off = kbyte + c * 16;
+    const bool in = off < kbytes;
+    i32x4 v[NLD];
 #pragma unroll
-    for (int p = 0; p < NLD; ++p) {
-      i32x4 v = {0, 0, 0, 0};
-      if (off < kbytes) v = *reinterpret_cast<const i32x4*>(ptr[p] + off);
-      *reinterpret_cast<i32x4*>(sbase + lds_off(r0 + RSTRIDE * p, c)) = v;
-    }
+    for (int p = 0; p < NLD; ++p) v[p] = *(GlobalChunk*)(ptr[p] + (in ? off : 0));
+#pragma unroll
+    for (int p = 0; p < NLD; ++p)
+      *reinterpret_cast<i32x4*>(sbase + lds_off(r0 + RSTRIDE * p, c)) = in ? v[p] : i32x4{0, 0, 0, 0};
   }
 };
 
@@ -168,18 +174,20 @@ struct BufRows {
     }
   }
 
+  // Every load is issued before the first LDS write (one memory round trip);
+  // chunks past kbytes get an out-of-range offset and read as zero.
   template <int RS>
   __device__ __forceinline__ void tail(int64_t kbyte, int64_t kbytes, char* sbase) const {
     const int c = threadIdx.x & 7;
     const int r0 = threadIdx.x >> 3;
     const int64_t off = kbyte + c * 16;
     const uint32_t rowoff = static_cast<uint32_t>(r0) * stride + static_cast<uint32_t>(off);
+    const bool in = off < kbytes;
+    i32x4 v[NLD];
 #pragma unroll
-    for (int p = 0; p < NLD; ++p) {
-      i32x4 v = {0, 0, 0, 0};
-      if (off < kbytes) v = fg_raw_buffer_load_b128(rsrc, rowoff + p * pstride, 0, 0);
-      *reinterpret_cast<i32x4*>(sbase + lds_off(r0 + RS * p, c)) = v;
-    }
+    for (int p = 0; p < NLD; ++p) v[p] = fg_raw_buffer_load_b128(rsrc, in ? rowoff + p * pstride : 0x80000000u, 0, 0);
+#pragma unroll
+    for (int p = 0; p < NLD; ++p) *reinterpret_cast<i32x4*>(sbase + lds_off(r0 + RS * p, c)) = v[p];
   }
 };
 
