@@ -47,7 +47,7 @@ def parse():
                          "(3 times); its HBM counters calibrate rocprofv3 FETCH_SIZE/WRITE_SIZE")
     ap.add_argument("--workload", default="gelu_clamp",
                     choices=["gelu_clamp", "lse", "silu_gn", "tiny_f32", "moe_prefill_bf16",
-                             "moe_prefill_e4m3", "moe_decode_bf16", "moe_decode_e4m3"],
+                             "moe_prefill_e4m3", "moe_decode_bf16", "moe_decode_e4m3", "moe_finalize"],
                     help="gelu_clamp (default) is the headline workload; the others are the "
                          "remaining configurations, measured the same way")
     return ap.parse_args()
@@ -323,6 +323,65 @@ def bench_moe(args, torch, np):
     return result
 
 
+def bench_finalize(args, torch, np):
+    """The standalone MoE finalize over the batch sizes of paper Table I
+    (top-4, H = 2880). Each launch moves a few MB, so launches are captured
+    back to back in one HIP graph and the graph is timed; per-launch time is
+    the graph time over the launches in it. The headline line is T = 128."""
+    from paper_2606_02963_amd import api
+    from paper_2606_02963_amd.synth import FINALIZE_BATCHES, FINALIZE_H, FINALIZE_K, make_finalize_inputs
+
+    reps = 50
+    H, k = FINALIZE_H, FINALIZE_K
+    sweep = {}
+    for T in FINALIZE_BATCHES:
+        bits = make_finalize_inputs(T)
+        y = torch.from_numpy(bits.view(np.int16)).view(torch.bfloat16).cuda()
+        out = torch.empty((T, H), dtype=torch.bfloat16, device="cuda")
+        api.moe_finalize(y, k, out=out)
+        torch.cuda.synchronize()
+        eager = out.clone()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                api.moe_finalize(y, k, out=out)
+        g.replay()
+        torch.cuda.synchronize()
+        if not torch.equal(out, eager):
+            raise RuntimeError("graph replay of moe_finalize differs from the eager launch")
+        settle(g.replay, min(args.warmup_seconds, 0.3), torch)
+        ms = time_steps(g.replay, max(args.steps // 5, 5), max(args.warmup // 5, 2), torch) / reps
+        nbytes = (T * k * H + T * H) * 2
+        sweep[T] = {"us": round(ms * 1e3, 3), "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1), "bytes": nbytes}
+    T = FINALIZE_BATCHES[-1]
+    head = sweep[T]
+    roof = {"bound": "hbm", "achieved": head["gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(head["gbs"] / PEAK_HBM_GBS, 4), "traffic": None,
+            "algorithmic_bytes_per_launch": head["bytes"]}
+    result = {
+        "metric": "MoE finalize effective HBM GB/s (paper Table I batch sweep)", "value": head["gbs"],
+        "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(head["us"] / 1e3, 6), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded: y_slot ~ N(0, 0.25); see "
+        "paper_2606_02963_amd/synth.py)",
+        "config": {"workload": f"MoE finalize y_slot[{T}x{k}, {H}] bf16 -> out[{T}, {H}] bf16, fp32 sum",
+                   "T": T, "H": H, "top_k": k, "launches_per_graph": reps},
+        "roofline": roof, "sweep": {str(t): v for t, v in sweep.items()}}
+    if not args.no_cpu_baseline:
+        from oracle import bf16_decode, ref_moe_finalize
+        y64 = bf16_decode(make_finalize_inputs(T))
+        t0, n = time.perf_counter(), 0
+        while time.perf_counter() - t0 < 1.0:
+            ref_moe_finalize(y64, k)
+            n += 1
+        sec = (time.perf_counter() - t0) / n
+        result["cpu_baseline"] = {"value": round(head["bytes"] / sec / 1e9, 3), "unit": "GB/s",
+                                  "cores": 1, "kind": "oracle",
+                                  "sample": f"the whole T={T} finalize, {n} repetitions in ~1 s",
+                                  "seconds": round(sec, 6)}
+    return result
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -343,6 +402,8 @@ def main():
     _lib.lib()   # fail loudly if the HIP library is missing
     if args.workload in MOE_WORKLOADS:
         result = bench_moe(args, torch, np)
+    elif args.workload == "moe_finalize":
+        result = bench_finalize(args, torch, np)
     else:
         result = bench_fgemm(args, torch, np)
     if args.copy_calibration_mb > 0:

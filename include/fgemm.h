@@ -198,6 +198,22 @@ fg_status moe_grouped_ffn(const moe_desc *d, const void *tokens,
                           void *workspace, size_t ws_bytes, void *stream);
 
 /*
+ * moe_finalize — the MoE finalize step on its own (paper §IV-A, the "MoE
+ * finalize" kernel of Table I; also the last launch of moe_grouped_ffn):
+ *   out[t, :] = Σ_{j = 0 .. top_k−1} y_slot[t·top_k + j, :]
+ * summed in fp32 in ascending j, rounded once to bf16 (nearest even).
+ *   y_slot  [T·top_k, H] bf16, row t·top_k + j = token t's j-th routed slot,
+ *           already multiplied by its routing weight (caller-owned, device).
+ *   out     [T, H] bf16 (caller-owned, device); must not overlap y_slot.
+ *   T ≥ 0 (0: nothing is enqueued), 1 ≤ top_k ≤ 8, H a multiple of 8.
+ * FG_ERR_INVALID_ARG for bad sizes or NULL pointers, FG_ERR_ALIGNMENT for H
+ * not a multiple of 8 or pointers not 16-byte aligned; nothing is enqueued
+ * on error.
+ */
+fg_status moe_finalize(const void *y_slot, void *out, int64_t T, int64_t H,
+                       int32_t top_k, void *stream);
+
+/*
  * fg_quantize_rows_e4m3 — the W8A8 path's activation quantiser as a
  * standalone call: for each of `rows` rows of `cols` bf16 values,
  * s = amax/448 (1 for an all-zero row) and q = e4m3fn(v/s) with

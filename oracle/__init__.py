@@ -25,12 +25,12 @@ forms, invariants, brute force (mpmath) and library special cases; none is
 from .codecs import (bf16_decode, bf16_encode_rne, e4m3_decode,
                      e4m3_encode_rne_sat, f32_round)
 from .fgemm import ref_fgemm, OPS
-from .moe import ref_route, ref_permute, ref_swiglu_clamped, ref_moe, ref_quant_rows_e4m3
+from .moe import ref_route, ref_permute, ref_swiglu_clamped, ref_moe, ref_moe_finalize, ref_quant_rows_e4m3
 from .compare import rel_err, ComparisonReport, compare
 
 __all__ = [
     "bf16_decode", "bf16_encode_rne", "e4m3_decode", "e4m3_encode_rne_sat",
     "f32_round", "ref_fgemm", "OPS", "ref_route", "ref_permute",
-    "ref_swiglu_clamped", "ref_moe", "ref_quant_rows_e4m3", "rel_err",
+    "ref_swiglu_clamped", "ref_moe", "ref_moe_finalize", "ref_quant_rows_e4m3", "rel_err",
     "ComparisonReport", "compare",
 ]

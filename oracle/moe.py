@@ -145,6 +145,22 @@ def _split_gate_up(G, I, interleaved):
     return G[:, :I], G[:, I:]
 
 
+def ref_moe_finalize(y_slot, k):
+    """The MoE finalize step (§IV-A, the "MoE finalize" kernel of Table I), as
+    the method declares it: y_slot [T·k, H] holds each token's k routed slot
+    outputs, already multiplied by their routing weights, row t·k + j for
+    slot j of token t; out[t] = Σ_j y_slot[t·k + j] over j = 0 .. k−1, in
+    ascending j. Exact in fp64 for the decoded bf16 inputs of the tests."""
+    y = np.asarray(y_slot, dtype=np.float64)
+    if y.shape[0] % k != 0:
+        raise ValueError("rows of y_slot must be a multiple of k")
+    T = y.shape[0] // k
+    out = np.zeros((T, y.shape[1]), dtype=np.float64)
+    for j in range(k):
+        out += y[j::k]
+    return out
+
+
 def ref_expert_rows(X, W_gu, W_d, storage="bf16", act_quant=False, alpha=1.702,
                     limit=7.0, interleaved=False, with_bound=False):
     """One expert's FFN over rows X [n, H] → y [n, H] (unweighted), fp64.

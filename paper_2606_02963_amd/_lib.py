@@ -71,6 +71,8 @@ def lib():
         L.moe_workspace_bytes.restype = sz
         L.moe_grouped_ffn.argtypes = [C.POINTER(MoeDesc)] + [vp] * 12 + [sz, vp]
         L.moe_grouped_ffn.restype = i32
+        L.moe_finalize.argtypes = [vp, vp, i64, i64, i32, vp]
+        L.moe_finalize.restype = i32
         L.fg_quantize_rows_e4m3.argtypes = [vp, i64, i64, vp, vp, vp]
         L.fg_quantize_rows_e4m3.restype = i32
         L.fg_status_str.argtypes = [i32]
@@ -186,3 +188,8 @@ def moe_grouped_ffn(desc, tokens, router_logits, w_gateup, w_down, s_gateup, s_d
 
 def fg_quantize_rows_e4m3(x, rows, cols, q, s, stream=None):
     _check(lib().fg_quantize_rows_e4m3(x, int(rows), int(cols), q, s, stream), "fg_quantize_rows_e4m3")
+
+
+def moe_finalize(y_slot, out, T, H, top_k, stream=None):
+    """out[t] = Σ_j y_slot[t·top_k + j] (bf16, fp32 sum in ascending j)."""
+    _check(lib().moe_finalize(y_slot, out, T, H, top_k, stream), "moe_finalize")

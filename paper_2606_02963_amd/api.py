@@ -119,3 +119,18 @@ def quantize_rows_e4m3(x, stream=None):
     s = torch.empty((rows,), dtype=torch.float32, device=x.device)
     _lib.fg_quantize_rows_e4m3(_dev(x, "x"), rows, cols, _dev(q, "q"), _dev(s, "s"), _stream(stream))
     return q, s
+
+
+def moe_finalize(y_slot, top_k, out=None, stream=None):
+    """MoE finalize: y_slot [T·top_k, H] bf16 (routing-weighted slot outputs,
+    row t·top_k + j) → out [T, H] bf16 = Σ_j y_slot[t·top_k + j], fp32 sum."""
+    S, H = y_slot.shape
+    if y_slot.dtype != torch.bfloat16:
+        raise TypeError("y_slot must be bf16")
+    if S % top_k != 0:
+        raise ValueError("y_slot rows must be a multiple of top_k")
+    T = S // top_k
+    if out is None:
+        out = torch.empty((T, H), dtype=torch.bfloat16, device=y_slot.device)
+    _lib.moe_finalize(_dev(y_slot, "y_slot"), _dev(out, "out"), T, H, top_k, _stream(stream))
+    return out

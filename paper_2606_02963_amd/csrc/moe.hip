@@ -530,30 +530,54 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
 }
 
 // ---------------------------------------------------------------------------
-// finalize: out[t, :] = Σ_j y_slot[t·k + j, :], j ascending, fp32 sum, bf16 out.
-// One thread per 8 consecutive columns of a token.
+// finalize: out[t, :] = Σ_j y_slot[t·k + j, :], j ascending, fp32 sum, bf16 out
+// (paper §IV-A, the MoE finalize kernel of Table I). One thread per 8
+// consecutive columns of a token; its K loads are all issued before the
+// first add, so a launch costs one memory round trip whatever K is.
 
+template <int K>
 __global__ __launch_bounds__(256) void moe_finalize_kernel(const uint16_t* y_slot, uint16_t* out, int T,
-                                                           int64_t H, int k) {
+                                                           int64_t H) {
   const int64_t cpt = H / 8;
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t t = idx / cpt, c = idx % cpt;
   if (t >= T) return;
+  i32x4 v[K];
+#pragma unroll
+  for (int j = 0; j < K; ++j) v[j] = *reinterpret_cast<const i32x4*>(y_slot + ((t * K + j) * H + c * 8));
   float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-  for (int j = 0; j < k; ++j) {
-    const i32x4 v = *reinterpret_cast<const i32x4*>(y_slot + ((t * k + j) * H + c * 8));
+#pragma unroll
+  for (int j = 0; j < K; ++j)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      acc[2 * q] += bf16_bits_to_f32((uint16_t)(v[q] & 0xffff));
-      acc[2 * q + 1] += bf16_bits_to_f32((uint16_t)((uint32_t)v[q] >> 16));
+      acc[2 * q] += bf16_bits_to_f32((uint16_t)(v[j][q] & 0xffff));
+      acc[2 * q + 1] += bf16_bits_to_f32((uint16_t)((uint32_t)v[j][q] >> 16));
     }
-  }
   i32x4 o;
 #pragma unroll
   for (int q = 0; q < 4; ++q)
     o[q] = (int)((uint32_t)f32_to_bf16_bits(acc[2 * q]) | ((uint32_t)f32_to_bf16_bits(acc[2 * q + 1]) << 16));
   *reinterpret_cast<i32x4*>(out + (t * H + c * 8)) = o;
 }
+
+// Enqueue the finalize for top_k = k (1 .. KMAX).
+static void launch_finalize(const void* y_slot, void* out, int64_t T, int64_t H, int k, hipStream_t s) {
+  const int64_t threads = T * (H / 8);
+  const dim3 grid((unsigned)((threads + 255) / 256)), block(256);
+  const uint16_t* y = static_cast<const uint16_t*>(y_slot);
+  uint16_t* o = static_cast<uint16_t*>(out);
+  switch (k) {
+    case 1: hipLaunchKernelGGL(moe_finalize_kernel<1>, grid, block, 0, s, y, o, (int)T, H); break;
+    case 2: hipLaunchKernelGGL(moe_finalize_kernel<2>, grid, block, 0, s, y, o, (int)T, H); break;
+    case 3: hipLaunchKernelGGL(moe_finalize_kernel<3>, grid, block, 0, s, y, o, (int)T, H); break;
+    case 4: hipLaunchKernelGGL(moe_finalize_kernel<4>, grid, block, 0, s, y, o, (int)T, H); break;
+    case 5: hipLaunchKernelGGL(moe_finalize_kernel<5>, grid, block, 0, s, y, o, (int)T, H); break;
+    case 6: hipLaunchKernelGGL(moe_finalize_kernel<6>, grid, block, 0, s, y, o, (int)T, H); break;
+    case 7: hipLaunchKernelGGL(moe_finalize_kernel<7>, grid, block, 0, s, y, o, (int)T, H); break;
+    default: hipLaunchKernelGGL(moe_finalize_kernel<8>, grid, block, 0, s, y, o, (int)T, H); break;
+  }
+}
+static_assert(KMAX == 8, "launch_finalize instantiates top_k 1 .. 8");
 
 __global__ __launch_bounds__(256) void fill_i32_kernel(int32_t* p, int n, int v) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -805,9 +829,20 @@ extern "C" fg_status moe_grouped_ffn(const moe_desc* d, const void* tokens, cons
     else launch_grouped<GBf16Small, EPI_DOWN>(g, S, s);
   }
 
-  const int64_t threads = d->T * (d->H / 8);
-  hipLaunchKernelGGL(moe_finalize_kernel, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s,
-                     reinterpret_cast<const uint16_t*>(ws + L.y), static_cast<uint16_t*>(out), T, d->H,
-                     d->top_k);
+  launch_finalize(ws + L.y, out, d->T, d->H, d->top_k, s);
+  return check_launch(fn);
+}
+
+extern "C" fg_status moe_finalize(const void* y_slot, void* out, int64_t T, int64_t H, int32_t top_k, void* stream) {
+  clear_error();
+  const char* fn = "moe_finalize";
+  if (T < 0 || T > 0x7fffffffLL || H <= 0 || H > (1 << 20))
+    return fail(FG_ERR_INVALID_ARG, "%s: bad T=%lld or H=%lld", fn, (long long)T, (long long)H);
+  if (top_k < 1 || top_k > KMAX) return fail(FG_ERR_INVALID_ARG, "%s: top_k=%d outside 1..%d", fn, top_k, KMAX);
+  if (H % 8 != 0) return fail(FG_ERR_ALIGNMENT, "%s: H must be a multiple of 8", fn);
+  if (T == 0) return FG_OK;
+  if (y_slot == nullptr || out == nullptr) return fail(FG_ERR_INVALID_ARG, "%s: NULL pointer", fn);
+  if (!aligned16(y_slot) || !aligned16(out)) return fail(FG_ERR_ALIGNMENT, "%s: pointers must be 16-byte aligned", fn);
+  launch_finalize(y_slot, out, T, H, top_k, static_cast<hipStream_t>(stream));
   return check_launch(fn);
 }

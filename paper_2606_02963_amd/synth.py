@@ -212,3 +212,28 @@ def make_moe_weights(spec, seed=0):
     """All experts stacked: w_gate_up [E,2I,H], w_down [E,H,I] (+ scales)."""
     parts = [make_moe_expert(spec, e, seed) for e in range(spec.E)]
     return {key: np.stack([p[key] for p in parts]) for key in parts[0]}
+
+
+# --------------------------------------------------------------------------
+# MoE finalize (the standalone kernel of paper §IV-A, Table I): batch sizes
+# 1 .. 128 of the gpt-oss-20b decode path, top-4, H = 2880.
+
+FINALIZE_BATCHES = (1, 4, 8, 16, 32, 64, 128)
+FINALIZE_H = 2880
+FINALIZE_K = 4
+
+
+def make_finalize_inputs(T, H=FINALIZE_H, k=FINALIZE_K, seed=0, exact=False):
+    """Routing-weighted slot outputs y_slot [T·k, H] as bf16 bits.
+
+    Default: N(0, 0.25), the scale of a weighted expert output. With
+    ``exact``, every value is ±(1 + u/128)·2^e with u in 0..127 and e in
+    −4..4 (each exactly a bf16 value), so that a sum of up to eight of them
+    needs at most 19 significant bits and is exact in fp32."""
+    rng = np.random.default_rng([seed, 2000 + T])
+    if not exact:
+        return to_bf16_bits(_normal(rng, (T * k, H), 0.25))
+    u = rng.integers(0, 128, (T * k, H))
+    e = rng.integers(-4, 5, (T * k, H))
+    sign = np.where(rng.random((T * k, H)) < 0.5, -1.0, 1.0)
+    return to_bf16_bits((sign * (1.0 + u / 128.0) * np.exp2(e)).astype(np.float32))

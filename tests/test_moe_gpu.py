@@ -13,11 +13,12 @@ import numpy as np
 import pytest
 import torch
 
-from oracle import bf16_decode, compare, e4m3_decode, ref_moe, ref_quant_rows_e4m3
+from oracle import bf16_decode, bf16_encode_rne, compare, e4m3_decode, ref_moe, ref_moe_finalize, ref_quant_rows_e4m3
 from paper_2606_02963_amd import _lib as L
 from paper_2606_02963_amd import api
-from paper_2606_02963_amd.synth import (MOE_SPECS, MoeSpec, make_moe_activations,
-                                        make_moe_weights, to_bf16_bits)
+from paper_2606_02963_amd.synth import (FINALIZE_BATCHES, FINALIZE_H, FINALIZE_K, MOE_SPECS, MoeSpec,
+                                        make_finalize_inputs, make_moe_activations, make_moe_weights,
+                                        to_bf16_bits)
 from tests.gpu_helpers import dev_bf16, dev_f32, dev_u8, host64, log, require_gpu
 
 pytestmark = pytest.mark.gpu
@@ -162,6 +163,63 @@ def test_quantize_rows_e4m3_bit_exact():
     q_ref, s_ref = ref_quant_rows_e4m3(x64)
     assert np.array_equal(s.cpu().numpy().astype(np.float64), s_ref)
     assert np.array_equal(q.cpu().numpy(), q_ref)
+
+
+def _finalize(bits, k):
+    y = dev_bf16(bits)
+    out = api.moe_finalize(y, k)
+    torch.cuda.synchronize()
+    return out.cpu().view(torch.int16).numpy().view(np.uint16)
+
+
+@pytest.mark.parametrize("T", FINALIZE_BATCHES)
+def test_moe_finalize_table_i_batches(T):
+    """The standalone finalize over the paper's batch sweep (top-4, H = 2880):
+    bit-exact against the exact sum rounded once to bf16 on inputs whose fp32
+    sum is exact, and within the bf16 tolerance on N(0, 0.25) inputs."""
+    require_gpu()
+    log(f"[finalize] T={T} H={FINALIZE_H} k={FINALIZE_K}")
+    bits = make_finalize_inputs(T, exact=True, seed=1)
+    got = _finalize(bits, FINALIZE_K)
+    want = bf16_encode_rne(ref_moe_finalize(bf16_decode(bits), FINALIZE_K))
+    assert np.array_equal(got, want)
+    bits = make_finalize_inputs(T, seed=2)
+    rep = compare(bf16_decode(_finalize(bits, FINALIZE_K)), ref_moe_finalize(bf16_decode(bits), FINALIZE_K), "bf16")
+    log(f"    {rep}")
+    assert rep.ok, rep
+
+
+@pytest.mark.parametrize("T,H,k", [(3, 8, 1), (5, 24, 3), (2, 136, 8), (7, 2880, 2)])
+def test_moe_finalize_edge_shapes(T, H, k):
+    """Minimum width (one 8-column chunk), odd T, k = 1 (a copy), k = 8 (the
+    largest top_k), and widths that are not a multiple of the workgroup."""
+    require_gpu()
+    log(f"[finalize] T={T} H={H} k={k}")
+    bits = make_finalize_inputs(T, H, k, seed=3, exact=True)
+    got = _finalize(bits, k)
+    assert np.array_equal(got, bf16_encode_rne(ref_moe_finalize(bf16_decode(bits), k)))
+    if k == 1:
+        assert np.array_equal(got, bits)
+
+
+def test_moe_finalize_errors_and_empty():
+    require_gpu()
+    y = torch.zeros((8, 16), dtype=torch.bfloat16, device="cuda")
+    out = torch.zeros((2, 16), dtype=torch.bfloat16, device="cuda")
+    L.moe_finalize(y.data_ptr(), out.data_ptr(), 0, 16, 4, None)          # T = 0: nothing enqueued
+    for args, status in [((2, 12, 4), L.FG_ERR_ALIGNMENT),                 # H not a multiple of 8
+                         ((2, 16, 9), L.FG_ERR_INVALID_ARG),               # top_k > 8
+                         ((2, 16, 0), L.FG_ERR_INVALID_ARG),
+                         ((-1, 16, 4), L.FG_ERR_INVALID_ARG)]:
+        with pytest.raises(L.FgError) as ei:
+            L.moe_finalize(y.data_ptr(), out.data_ptr(), *args, None)
+        assert ei.value.status == status
+    with pytest.raises(L.FgError) as ei:
+        L.moe_finalize(y.data_ptr() + 2, out.data_ptr(), 2, 16, 4, None)   # misaligned
+    assert ei.value.status == L.FG_ERR_ALIGNMENT
+    with pytest.raises(L.FgError) as ei:
+        L.moe_finalize(None, out.data_ptr(), 2, 16, 4, None)
+    assert ei.value.status == L.FG_ERR_INVALID_ARG
 
 
 def test_moe_validation_errors():

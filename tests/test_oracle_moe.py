@@ -7,7 +7,9 @@ forms (arange and all-equal logits); the permutation against its definition
 mpmath; the whole block against a token-order brute force in mpmath that
 never builds the permutation, against the dense FFN it reduces to at E = 1,
 k = 1, and against the identical-experts and zero-W_down closed forms. The
-fp8 activation quantiser is pinned by the e4m3 grid and by its extreme code."""
+fp8 activation quantiser is pinned by the e4m3 grid and by its extreme code.
+The standalone finalize is pinned by an mpmath brute force over (token,
+column, slot), the k = 1 identity and an exactly cancelling slot pair."""
 
 import math
 
@@ -18,7 +20,7 @@ import pytest
 import oracle.moe as om
 from oracle.codecs import bf16_decode, bf16_encode_rne, e4m3_decode
 from oracle.fgemm import ref_fgemm
-from oracle.moe import (ref_moe, ref_permute, ref_quant_rows_e4m3, ref_route,
+from oracle.moe import (ref_moe, ref_moe_finalize, ref_permute, ref_quant_rows_e4m3, ref_route,
                         ref_swiglu_clamped)
 from paper_2606_02963_amd.synth import MoeSpec, make_moe_activations, make_moe_weights
 
@@ -312,3 +314,39 @@ def test_storage_deviation_bound():
     r3 = ref_moe(x, rng.standard_normal((6, 2)), (Wgu, Wd), 2, storage="e4m3")
     assert r3["out"].shape == r2["out"].shape
     assert FRAGILE_REL < 1e-4
+
+
+def test_finalize_bruteforce_via(fn=ref_moe_finalize):
+    """out[t, h] = Σ_j y_slot[t·k + j, h], summed one element at a time in
+    mpmath, with slot rows of very different magnitudes."""
+    rng = np.random.default_rng(23)
+    T, H, k = 3, 5, 3
+    y = bf16_decode(bf16_encode_rne(rng.standard_normal((T * k, H)) * np.exp2(rng.integers(-6, 7, (T * k, 1)))))
+    got = fn(y, k)
+    assert got.shape == (T, H)
+    for t in range(T):
+        for h in range(H):
+            want = mp.fsum(mp.mpf(float(y[t * k + j, h])) for j in range(k))
+            assert got[t, h] == float(want), (t, h)
+
+
+def test_finalize_identity_and_cancellation():
+    rng = np.random.default_rng(24)
+    y = bf16_decode(bf16_encode_rne(rng.standard_normal((4, 16))))
+    np.testing.assert_array_equal(ref_moe_finalize(y, 1), y)            # k = 1: each slot is its token
+    pair = np.concatenate([y[:, None, :], -y[:, None, :]], axis=1).reshape(8, 16)
+    np.testing.assert_array_equal(ref_moe_finalize(pair, 2), np.zeros((4, 16)))
+    with pytest.raises(ValueError):
+        ref_moe_finalize(y[:3], 2)
+
+
+def test_finalize_planted_stride_mistake_is_caught():
+    """Slots read with the token-major stride swapped (row j·T + t instead of
+    t·k + j) fail the brute-force pin."""
+    def wrong_stride(y_slot, k):
+        y = np.asarray(y_slot, dtype=np.float64)
+        T = y.shape[0] // k
+        return sum(y[j * T:(j + 1) * T] for j in range(k))
+    with pytest.raises(AssertionError):
+        test_finalize_bruteforce_via(wrong_stride)
+
