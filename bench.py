@@ -47,7 +47,7 @@ def parse():
                          "(3 times); its HBM counters calibrate rocprofv3 FETCH_SIZE/WRITE_SIZE")
     ap.add_argument("--workload", default="gelu_clamp",
                     choices=["gelu_clamp", "lse", "silu_gn", "tiny_f32", "moe_prefill_bf16",
-                             "moe_prefill_e4m3", "moe_decode_bf16", "moe_decode_e4m3", "moe_finalize"],
+                             "moe_prefill_e4m3", "moe_decode_bf16", "moe_decode_e4m3", "moe_finalize", "add_rmsnorm"],
                     help="gelu_clamp (default) is the headline workload; the others are the "
                          "remaining configurations, measured the same way")
     return ap.parse_args()
@@ -382,6 +382,64 @@ def bench_finalize(args, torch, np):
     return result
 
 
+def bench_add_rmsnorm(args, torch, np):
+    """The fused residual add + RMSNorm over the batch sizes of paper Table I
+    (H = 2880, eps = 1e-5), timed like the finalize: launches captured back
+    to back in one HIP graph. Each launch reads x, the residual and the
+    weight and writes the residual and out; the headline line is T = 128.
+    The residual is updated in place, so the graph's launches chain (each
+    adds x once more), which changes the values but not the work."""
+    from paper_2606_02963_amd import api
+    from paper_2606_02963_amd.synth import FINALIZE_BATCHES, NORM_H, make_norm_inputs
+
+    reps = 50
+    H = NORM_H
+    dev = torch.device("cuda", 0)
+    bf = lambda a: torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to(dev)  # noqa: E731
+    sweep = {}
+    for T in FINALIZE_BATCHES:
+        x, r, w = (bf(a) for a in make_norm_inputs(T))
+        out = torch.empty((T, H), dtype=torch.bfloat16, device=dev)
+        api.add_rmsnorm(x, r, w, out=out)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                api.add_rmsnorm(x, r, w, out=out)
+        settle(g.replay, min(args.warmup_seconds, 0.3), torch)
+        ms = time_steps(g.replay, max(args.steps // 5, 5), max(args.warmup // 5, 2), torch) / reps
+        nbytes = 4 * T * H * 2 + H * 2
+        sweep[T] = {"us": round(ms * 1e3, 3), "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1), "bytes": nbytes}
+    T = FINALIZE_BATCHES[-1]
+    head = sweep[T]
+    roof = {"bound": "hbm", "achieved": head["gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(head["gbs"] / PEAK_HBM_GBS, 4), "traffic": None,
+            "algorithmic_bytes_per_launch": head["bytes"]}
+    result = {
+        "metric": "fused add + RMSNorm effective HBM GB/s (paper Table I batch sweep)", "value": head["gbs"],
+        "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(head["us"] / 1e3, 6), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded: x ~ N(0,1), residual ~ N(0,4), weight ~ U(0.5,1.5); see "
+                "paper_2606_02963_amd/synth.py)",
+        "config": {"workload": f"residual add + RMSNorm, x/residual[{T}, {H}] bf16, eps 1e-5",
+                   "T": T, "H": H, "launches_per_graph": reps},
+        "roofline": roof, "sweep": {str(t): v for t, v in sweep.items()}}
+    if not args.no_cpu_baseline:
+        from oracle import bf16_decode, ref_add_rmsnorm
+        x, r, w = (bf16_decode(a) for a in make_norm_inputs(T))
+        t0, n = time.perf_counter(), 0
+        while time.perf_counter() - t0 < 1.0:
+            ref_add_rmsnorm(x, r, w, 1e-5)
+            n += 1
+        sec = (time.perf_counter() - t0) / n
+        result["cpu_baseline"] = {"value": round(head["bytes"] / sec / 1e9, 3), "unit": "GB/s",
+                                  "cores": 1, "kind": "oracle",
+                                  "sample": f"the whole T={T} step, {n} repetitions in ~1 s",
+                                  "seconds": round(sec, 6)}
+    return result
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -404,6 +462,8 @@ def main():
         result = bench_moe(args, torch, np)
     elif args.workload == "moe_finalize":
         result = bench_finalize(args, torch, np)
+    elif args.workload == "add_rmsnorm":
+        result = bench_add_rmsnorm(args, torch, np)
     else:
         result = bench_fgemm(args, torch, np)
     if args.copy_calibration_mb > 0:

@@ -214,6 +214,23 @@ fg_status moe_finalize(const void *y_slot, void *out, int64_t T, int64_t H,
                        int32_t top_k, void *stream);
 
 /*
+ * add_rmsnorm — fused residual add + RMSNorm (paper §IV-A, "Fused Add +
+ * RMSNorm" in Table I), for each of the T rows of H channels:
+ *   s = x + residual  (fp32; exact for bf16 inputs)
+ *   residual ← bf16(s)                                   (in place)
+ *   out = bf16(s / sqrt(mean_h s² + eps) · weight)        (s before rounding)
+ *   x [T, H] bf16; residual [T, H] bf16, read and overwritten; weight [H]
+ *   bf16; out [T, H] bf16. All caller-owned device memory; out must not
+ *   overlap x or residual. T ≥ 0 (0: nothing is enqueued); H a multiple of
+ *   8 and at most 4096; eps finite and ≥ 0 (gpt-oss uses 1e-5).
+ * FG_ERR_INVALID_ARG for bad sizes, eps or NULL pointers, FG_ERR_ALIGNMENT
+ * for H not a multiple of 8 or pointers not 16-byte aligned,
+ * FG_ERR_UNSUPPORTED for H above 4096; nothing is enqueued on error.
+ */
+fg_status add_rmsnorm(const void *x, void *residual, const void *weight,
+                      void *out, int64_t T, int64_t H, float eps, void *stream);
+
+/*
  * fg_quantize_rows_e4m3 — the W8A8 path's activation quantiser as a
  * standalone call: for each of `rows` rows of `cols` bf16 values,
  * s = amax/448 (1 for an all-zero row) and q = e4m3fn(v/s) with

@@ -26,11 +26,12 @@ from .codecs import (bf16_decode, bf16_encode_rne, e4m3_decode,
                      e4m3_encode_rne_sat, f32_round)
 from .fgemm import ref_fgemm, OPS
 from .moe import ref_route, ref_permute, ref_swiglu_clamped, ref_moe, ref_moe_finalize, ref_quant_rows_e4m3
+from .norm import ref_add_rmsnorm
 from .compare import rel_err, ComparisonReport, compare
 
 __all__ = [
     "bf16_decode", "bf16_encode_rne", "e4m3_decode", "e4m3_encode_rne_sat",
     "f32_round", "ref_fgemm", "OPS", "ref_route", "ref_permute",
-    "ref_swiglu_clamped", "ref_moe", "ref_moe_finalize", "ref_quant_rows_e4m3", "rel_err",
+    "ref_swiglu_clamped", "ref_moe", "ref_moe_finalize", "ref_quant_rows_e4m3", "ref_add_rmsnorm", "rel_err",
     "ComparisonReport", "compare",
 ]

@@ -73,6 +73,8 @@ def lib():
         L.moe_grouped_ffn.restype = i32
         L.moe_finalize.argtypes = [vp, vp, i64, i64, i32, vp]
         L.moe_finalize.restype = i32
+        L.add_rmsnorm.argtypes = [vp, vp, vp, vp, i64, i64, C.c_float, vp]
+        L.add_rmsnorm.restype = i32
         L.fg_quantize_rows_e4m3.argtypes = [vp, i64, i64, vp, vp, vp]
         L.fg_quantize_rows_e4m3.restype = i32
         L.fg_status_str.argtypes = [i32]
@@ -193,3 +195,8 @@ def fg_quantize_rows_e4m3(x, rows, cols, q, s, stream=None):
 def moe_finalize(y_slot, out, T, H, top_k, stream=None):
     """out[t] = Σ_j y_slot[t·top_k + j] (bf16, fp32 sum in ascending j)."""
     _check(lib().moe_finalize(y_slot, out, T, H, top_k, stream), "moe_finalize")
+
+
+def add_rmsnorm(x, residual, weight, out, T, H, eps, stream=None):
+    """residual <- bf16(x + residual); out = bf16(RMSNorm(x + residual) * weight)."""
+    _check(lib().add_rmsnorm(x, residual, weight, out, T, H, eps, stream), "add_rmsnorm")

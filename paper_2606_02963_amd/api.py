@@ -134,3 +134,17 @@ def moe_finalize(y_slot, top_k, out=None, stream=None):
         out = torch.empty((T, H), dtype=torch.bfloat16, device=y_slot.device)
     _lib.moe_finalize(_dev(y_slot, "y_slot"), _dev(out, "out"), T, H, top_k, _stream(stream))
     return out
+
+
+def add_rmsnorm(x, residual, weight, eps=1e-5, out=None, stream=None):
+    """Fused residual add + RMSNorm on bf16 [T, H] rows: residual is updated
+    in place to x + residual and out = RMSNorm(x + residual)·weight."""
+    T, H = x.shape
+    for name, t in (("x", x), ("residual", residual), ("weight", weight)):
+        if t.dtype != torch.bfloat16:
+            raise TypeError(f"{name} must be bf16")
+    if out is None:
+        out = torch.empty((T, H), dtype=torch.bfloat16, device=x.device)
+    _lib.add_rmsnorm(_dev(x, "x"), _dev(residual, "residual"), _dev(weight, "weight"), _dev(out, "out"),
+                     T, H, eps, _stream(stream))
+    return out

@@ -237,3 +237,20 @@ def make_finalize_inputs(T, H=FINALIZE_H, k=FINALIZE_K, seed=0, exact=False):
     e = rng.integers(-4, 5, (T * k, H))
     sign = np.where(rng.random((T * k, H)) < 0.5, -1.0, 1.0)
     return to_bf16_bits((sign * (1.0 + u / 128.0) * np.exp2(e)).astype(np.float32))
+
+
+# --------------------------------------------------------------------------
+# Fused residual add + RMSNorm (paper §IV-A, Table I): the same batch sizes,
+# hidden size 2880.
+
+NORM_H = 2880
+
+
+def make_norm_inputs(T, H=NORM_H, seed=0):
+    """x [T, H] ~ N(0, 1) (a layer output), residual [T, H] ~ N(0, 4) (the
+    residual stream) and weight [H] ~ U(0.5, 1.5), as bf16 bits."""
+    rng = np.random.default_rng([seed, 3000 + T])
+    x = to_bf16_bits(_normal(rng, (T, H), 1.0))
+    r = to_bf16_bits(_normal(rng, (T, H), 4.0))
+    w = to_bf16_bits((rng.random(H, dtype=np.float32) + np.float32(0.5)).astype(np.float32))
+    return x, r, w
