@@ -10,14 +10,21 @@ accumulation and post-processing. Fusion only reschedules these operations,
 so the oracle is their plain definition, composed in the order given:
 
   1. z = x·Wᵀ (+ b)                    — one fp64 matmul (library dgemm)
-  2. each elementwise op, in order     — SCALE, ADD, RELU, GELU_TANH, SILU, CLAMP
+  2. each elementwise op, in order     — SCALE, ADD, RELU, GELU_TANH, SILU,
+                                         CLAMP, MISH, LEAKY_RELU
   3. an optional terminal reduction    — row LogSumExp (one value per row) or
                                          GroupNorm over contiguous channel groups
+  4. elementwise ops after the reduction, in order (per element after
+     GroupNorm, per row value after LogSumExp): Table III chains such as
+     GroupNorm → LeakyReLU → Sum, GroupNorm → Swish → Mul → Swish, and
+     LogSumExp → Mish
 
 Definitions used (standard forms; the paper names the ops, not formulas):
   GELU_TANH(u) = ½·u·(1 + tanh(√(2/π)·(u + 0.044715·u³)))   (Hendrycks & Gimpel, tanh form)
   SILU(u)      = u / (1 + e^(−u))                              (Swish with β = 1)
   CLAMP(u)     = min(max(u, lo), hi)
+  MISH(u)      = u·tanh(ln(1 + e^u))                            (Misra 2019)
+  LEAKY_RELU(u)= u for u ≥ 0, a·u otherwise                     (slope a)
   LSE(row)     = M + ln Σ_n e^(z_n − M),  M = max_n z_n
   GroupNorm    : groups are contiguous channel blocks of N/G channels; per
                  row and group, μ = mean, σ² = mean((z − μ)²) (biased);
@@ -30,7 +37,7 @@ import math
 
 import numpy as np
 
-OPS = ("scale", "add", "relu", "gelu_tanh", "silu", "clamp")
+OPS = ("scale", "add", "relu", "gelu_tanh", "silu", "clamp", "mish", "leaky_relu")
 
 _SQRT_2_OVER_PI = math.sqrt(2.0 / math.pi)
 
@@ -50,6 +57,11 @@ def _silu(u):
     return out
 
 
+def _mish(u):
+    # softplus = ln(1 + e^u) = logaddexp(0, u), which overflows for no u
+    return u * np.tanh(np.logaddexp(0.0, u))
+
+
 def apply_op(z, op):
     """Apply one elementwise tail op, given as (kind, a, b), in fp64."""
     kind, a, b = (tuple(op) + (0.0, 0.0))[:3]
@@ -65,6 +77,10 @@ def apply_op(z, op):
         return _silu(z)
     if kind == "clamp":
         return np.minimum(np.maximum(z, a), b)
+    if kind == "mish":
+        return _mish(z)
+    if kind == "leaky_relu":
+        return np.where(z >= 0.0, z, a * z)
     raise ValueError(f"unknown op {kind!r}")
 
 
@@ -87,13 +103,14 @@ def group_norm(z, groups, eps, gamma, beta):
 
 
 def ref_fgemm(x, W, b=None, ops=(), reduction=None, gn_groups=None, gn_eps=1e-5,
-              gamma=None, beta=None):
+              gamma=None, beta=None, post_ops=()):
     """Plain definition of the fused linear + tail, in fp64.
 
     x: [M, K], W: [N, K] (nn.Linear layout), b: [N] or None — all fp64 arrays
     holding the exact values the kernel reads (decoded bf16 / fp32).
     ops: sequence of (kind, a, b) applied in order after the bias.
     reduction: None, "lse" (returns [M]) or "groupnorm" (returns [M, N]).
+    post_ops: (kind, a, b) ops applied in order to the reduction's result.
     """
     x = np.asarray(x, dtype=np.float64)
     W = np.asarray(W, dtype=np.float64)
@@ -105,11 +122,17 @@ def ref_fgemm(x, W, b=None, ops=(), reduction=None, gn_groups=None, gn_eps=1e-5,
     for op in ops:
         z = apply_op(z, op)
     if reduction is None:
+        if post_ops:
+            raise ValueError("post_ops need a reduction")
         return z
     if reduction == "lse":
-        return row_logsumexp(z)
-    if reduction == "groupnorm":
-        return group_norm(z, gn_groups, gn_eps,
-                          np.asarray(gamma, dtype=np.float64),
-                          np.asarray(beta, dtype=np.float64))
-    raise ValueError(f"unknown reduction {reduction!r}")
+        y = row_logsumexp(z)
+    elif reduction == "groupnorm":
+        y = group_norm(z, gn_groups, gn_eps,
+                       np.asarray(gamma, dtype=np.float64),
+                       np.asarray(beta, dtype=np.float64))
+    else:
+        raise ValueError(f"unknown reduction {reduction!r}")
+    for op in post_ops:
+        y = apply_op(y, op)
+    return y

@@ -49,10 +49,14 @@ def _mp_apply(u, op):
         return _mp_silu(u)
     if kind == "clamp":
         return min(max(u, mp.mpf(op[1])), mp.mpf(op[2]))
+    if kind == "mish":
+        return u * mp.tanh(mp.log(1 + mp.exp(u)))
+    if kind == "leaky_relu":
+        return u if u >= 0 else mp.mpf(op[1]) * u
     raise ValueError(kind)
 
 
-def _mp_fgemm(x, W, b, ops, reduction=None, groups=0, eps=1e-5, gamma=None, beta=None):
+def _mp_fgemm(x, W, b, ops, reduction=None, groups=0, eps=1e-5, gamma=None, beta=None, post_ops=()):
     M, K = x.shape
     N = W.shape[0]
     z = [[mp.fsum(mp.mpf(float(x[m, k])) * mp.mpf(float(W[n, k])) for k in range(K))
@@ -60,7 +64,10 @@ def _mp_fgemm(x, W, b, ops, reduction=None, groups=0, eps=1e-5, gamma=None, beta
     for op in ops:
         z = [[_mp_apply(v, op) for v in row] for row in z]
     if reduction == "lse":
-        return [mp.log(mp.fsum(mp.exp(v) for v in row)) for row in z]
+        out = [mp.log(mp.fsum(mp.exp(v) for v in row)) for row in z]
+        for op in post_ops:
+            out = [_mp_apply(v, op) for v in out]
+        return out
     if reduction == "groupnorm":
         gs = N // groups
         out = []
@@ -72,8 +79,11 @@ def _mp_fgemm(x, W, b, ops, reduction=None, groups=0, eps=1e-5, gamma=None, beta
                 var = mp.fsum((v - mu) ** 2 for v in seg) / gs
                 for i, v in enumerate(seg):
                     n = g * gs + i
-                    r.append((v - mu) / mp.sqrt(var + mp.mpf(eps)) * mp.mpf(float(gamma[n]))
-                             + mp.mpf(float(beta[n])))
+                    y = ((v - mu) / mp.sqrt(var + mp.mpf(eps)) * mp.mpf(float(gamma[n]))
+                         + mp.mpf(float(beta[n])))
+                    for op in post_ops:
+                        y = _mp_apply(y, op)
+                    r.append(y)
             out.append(r)
         return out
     return z
@@ -110,6 +120,47 @@ def test_bruteforce_mpmath(ops, red):
     want = np.array([[float(v) for v in r] for r in want]) if red != "lse" \
         else np.array([float(v) for v in want])
     np.testing.assert_allclose(got, want, rtol=1e-13, atol=1e-14)
+
+
+# Table III tail patterns: elementwise ops before and after the reduction
+POST_TAILS = [
+    ((("scale", 0.5),), "lse", (("mish",),)),                                     # Scale → LSE → Mish
+    ((), "groupnorm", (("silu",), ("scale", 1.5), ("silu",))),                    # GN → Swish → Mul → Swish
+    ((), "groupnorm", (("leaky_relu", 0.01), ("scale", 2.0))),                    # GN → LReLU → Sum
+    ((("silu",), ("add", 0.25)), "groupnorm", ()),                                # Swish → Sum → GN
+    ((("mish",), ("leaky_relu", 0.2)), None, ()),
+]
+
+
+@pytest.mark.parametrize("ops,red,post", POST_TAILS)
+def test_bruteforce_mpmath_post_ops(ops, red, post):
+    x, W, b = _tiny_bf16(3, 8, 8, seed=11 + len(ops) + len(post), scale=2.0)
+    kw = {}
+    if red == "groupnorm":
+        rng = np.random.default_rng(10)
+        kw = dict(gn_groups=2, gn_eps=1e-5, gamma=rng.random(8) + 0.5, beta=rng.standard_normal(8) * 0.1)
+    got = ref_fgemm(x, W, b, ops, red, post_ops=post, **kw)
+    want = _mp_fgemm(x, W, b, ops, red, kw.get("gn_groups", 0), 1e-5, kw.get("gamma"), kw.get("beta"), post)
+    want = np.array([[float(v) for v in r] for r in want]) if red != "lse" \
+        else np.array([float(v) for v in want])
+    np.testing.assert_allclose(got, want, rtol=1e-13, atol=1e-14)
+
+
+def test_mish_and_leaky_relu_closed_forms_and_torch():
+    u = torch.linspace(-30, 30, 6001, dtype=torch.float64)
+    un = u.numpy()
+    np.testing.assert_allclose(of.apply_op(un, ("mish",)), F.mish(u).numpy(), rtol=1e-14, atol=1e-15)
+    np.testing.assert_array_equal(of.apply_op(un, ("leaky_relu", 0.01)),
+                                  F.leaky_relu(u, 0.01).numpy())
+    assert of.apply_op(np.array([0.0]), ("mish",))[0] == 0.0
+    big = np.array([40.0, 700.0])
+    np.testing.assert_array_equal(of.apply_op(big, ("mish",)), big)            # tanh(softplus) = 1 in fp64
+    # slope: f(-t) = -a·t, f(t) = t
+    t = np.array([0.5, 3.0])
+    np.testing.assert_array_equal(of.apply_op(-t, ("leaky_relu", 0.25)), -0.25 * t)
+    np.testing.assert_array_equal(of.apply_op(t, ("leaky_relu", 0.25)), t)
+    with pytest.raises(ValueError):
+        ref_fgemm(np.eye(2), np.eye(2), None, (), None, post_ops=(("relu",),))
 
 
 # ---------------------------------------------------------------- closed forms
@@ -256,13 +307,17 @@ def _pins_pass():
     test_lse_invariants_and_torch()
     test_groupnorm_moments_with_unit_affine()
     test_groupnorm_affine_invariance_and_torch()
+    for ops, red, post in POST_TAILS:
+        test_bruteforce_mpmath_post_ops(ops, red, post)
+    test_mish_and_leaky_relu_closed_forms_and_torch()
 
 
 def test_pins_catch_planted_mistakes(monkeypatch):
     """Plant plausible mistakes in the oracle (on the CPU) and require that
     at least one pin fails for each: a wrong GELU constant, a dropped
     max-shift in LSE, unbiased variance in GroupNorm, eps outside the sqrt,
-    and a transposed weight operand."""
+    Mish with ReLU in place of softplus, post-reduction ops applied before
+    the reduction, and a transposed weight operand."""
     good_gelu = of._gelu_tanh
     mutants = {
         "gelu_const": ("_gelu_tanh", lambda u: 0.5 * u * (1 + np.tanh(of._SQRT_2_OVER_PI * (u + 0.0447 * u ** 3)))),
@@ -276,6 +331,7 @@ def test_pins_catch_planted_mistakes(monkeypatch):
             ((z.reshape(z.shape[0], G, -1) - z.reshape(z.shape[0], G, -1).mean(-1, keepdims=True))
              / (np.sqrt(z.reshape(z.shape[0], G, -1).var(-1, keepdims=True)) + eps)).reshape(z.shape) * g + b)),
         "silu_sign": ("_silu", lambda u: u / (1 + np.exp(u))),
+        "mish_relu_softplus": ("_mish", lambda u: u * np.tanh(np.maximum(u, 0.0))),
     }
     assert good_gelu is of._gelu_tanh
     for name, (attr, fn) in mutants.items():
@@ -283,6 +339,26 @@ def test_pins_catch_planted_mistakes(monkeypatch):
             m.setattr(of, attr, fn)
             with pytest.raises(AssertionError):
                 _pins_pass()
+    # post ops applied before the reduction instead of after it
+    good_ref = of.ref_fgemm
+
+    def post_before(x, W, b=None, ops=(), reduction=None, post_ops=(), **kw):
+        return good_ref(x, W, b, tuple(ops) + tuple(post_ops), reduction, **kw)
+    with monkeypatch.context() as m:
+        m.setattr(of, "ref_fgemm", post_before)
+        with pytest.raises(AssertionError):
+            for ops, red, post in POST_TAILS[:3]:
+                x, W, b = _tiny_bf16(3, 8, 8, seed=11 + len(ops) + len(post), scale=2.0)
+                kw = {}
+                if red == "groupnorm":
+                    rng = np.random.default_rng(10)
+                    kw = dict(gn_groups=2, gn_eps=1e-5, gamma=rng.random(8) + 0.5, beta=rng.standard_normal(8) * 0.1)
+                got = of.ref_fgemm(x, W, b, ops, red, post_ops=post, **kw)
+                want = _mp_fgemm(x, W, b, ops, red, kw.get("gn_groups", 0), 1e-5, kw.get("gamma"),
+                                 kw.get("beta"), post)
+                want = np.array([[float(v) for v in r] for r in want]) if red != "lse" \
+                    else np.array([float(v) for v in want])
+                np.testing.assert_allclose(got, want, rtol=1e-13, atol=1e-14)
     # transposed operand (x·W instead of x·Wᵀ, square W): the brute force disagrees
     x, W, b = _tiny_bf16(3, 8, 8, seed=1)
     bad = ref_fgemm(x, W.T, b, TAILS[0][0])
