@@ -12,7 +12,9 @@ roofline fraction against the dense bf16 MFMA peak, the unfused sequence
 it, and the fp64 CPU oracle timed on a bounded sample of rows.
 
 Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
-                       [--workload gelu_clamp|lse|silu_gn|tiny_f32|moe_{prefill,decode}_{bf16,e4m3}]
+                       [--workload gelu_clamp|lse|silu_gn|tiny_f32|scale_lse_mish|gn_swish_mul_swish|
+                                   gn_lrelu_sum|swish_sum_gn|moe_{prefill,decode}_{bf16,e4m3}|
+                                   moe_finalize|add_rmsnorm]
 """
 
 import argparse
@@ -46,7 +48,8 @@ def parse():
                     help="after the measurement, run a plain device-to-device copy of this many MiB "
                          "(3 times); its HBM counters calibrate rocprofv3 FETCH_SIZE/WRITE_SIZE")
     ap.add_argument("--workload", default="gelu_clamp",
-                    choices=["gelu_clamp", "lse", "silu_gn", "tiny_f32", "moe_prefill_bf16",
+                    choices=["gelu_clamp", "lse", "silu_gn", "tiny_f32", "scale_lse_mish",
+                             "gn_swish_mul_swish", "gn_lrelu_sum", "swish_sum_gn", "moe_prefill_bf16",
                              "moe_prefill_e4m3", "moe_decode_bf16", "moe_decode_e4m3", "moe_finalize", "add_rmsnorm"],
                     help="gelu_clamp (default) is the headline workload; the others are the "
                          "remaining configurations, measured the same way")
@@ -98,10 +101,16 @@ def time_steps(fn, steps, warmup, torch):
 
 
 FGEMM_WORKLOADS = {"gelu_clamp": "bf16_gelu_clamp", "lse": "bf16_lse", "silu_gn": "bf16_silu_gn",
-                   "tiny_f32": "tiny_f32_relu_x2"}
+                   "tiny_f32": "tiny_f32_relu_x2", "scale_lse_mish": "bf16_scale_lse_mish",
+                   "gn_swish_mul_swish": "bf16_gn_swish_mul_swish", "gn_lrelu_sum": "bf16_gn_lrelu_sum",
+                   "swish_sum_gn": "bf16_swish_sum_gn"}
 MOE_WORKLOADS = {"moe_prefill_bf16", "moe_prefill_e4m3", "moe_decode_bf16", "moe_decode_e4m3"}
 TAIL_TEXT = {"bf16_gelu_clamp": "(x0.5, GELU_tanh, clamp[-1,1])", "bf16_lse": "(-0.25, row logsumexp)",
-             "bf16_silu_gn": "(SiLU, GroupNorm 32x128)", "tiny_f32_relu_x2": "(ReLU, x2)"}
+             "bf16_silu_gn": "(SiLU, GroupNorm 32x128)", "tiny_f32_relu_x2": "(ReLU, x2)",
+             "bf16_scale_lse_mish": "(x2, row logsumexp, Mish)",
+             "bf16_gn_swish_mul_swish": "(GroupNorm 32x128, SiLU, x1.5, SiLU)",
+             "bf16_gn_lrelu_sum": "(GroupNorm 32x128, LeakyReLU 0.01, x+x)",
+             "bf16_swish_sum_gn": "(SiLU, +0.25, GroupNorm 32x128)"}
 
 
 def base_result(args, metric_value, ms, dtype, data, config, roofline):
@@ -133,13 +142,13 @@ def bench_fgemm(args, torch, np):
     out_dt = torch.float32 if spec.out == "f32" else torch.bfloat16
     out = torch.empty((spec.M,) if spec.reduction == "lse" else (spec.M, spec.N), dtype=out_dt, device=dev)
     plan = api.get_plan(spec.M, spec.N, spec.K, spec.dtype, spec.out, True, spec.ops, spec.reduction,
-                        spec.gn_groups, spec.gn_eps)
+                        spec.gn_groups, spec.gn_eps, spec.post_ops)
     info = plan.info()
     ws = torch.empty(max(plan.workspace_bytes(), 16), dtype=torch.uint8, device=dev)
 
     def fused():
         api.linear_epilogue(x, W, b, spec.ops, spec.reduction, spec.gn_groups, spec.gn_eps, g, be,
-                            out_dtype=spec.out, out=out, workspace=ws)
+                            out_dtype=spec.out, out=out, workspace=ws, post_ops=spec.post_ops)
 
     settle(fused, args.warmup_seconds, torch)
     ms = time_steps(fused, args.steps, args.warmup, torch)
@@ -166,10 +175,8 @@ def bench_fgemm(args, torch, np):
         tdt = torch.float32 if spec.dtype == "f32" else torch.bfloat16
         bb = b.to(tdt)
 
-        def unfused():
-            z = torch.mm(x, W.t())
-            z = z + bb
-            for op in spec.ops:
+        def eager_ops(z, ops):
+            for op in ops:
                 if op[0] == "scale":
                     z = z * op[1]
                 elif op[0] == "add":
@@ -182,11 +189,20 @@ def bench_fgemm(args, torch, np):
                     z = F.silu(z)
                 elif op[0] == "clamp":
                     z = torch.clamp(z, op[1], op[2])
-            if spec.reduction == "lse":
-                return torch.logsumexp(z.float(), dim=1)
-            if spec.reduction == "groupnorm":
-                return F.group_norm(z, spec.gn_groups, g.to(tdt), be.to(tdt), spec.gn_eps)
+                elif op[0] == "mish":
+                    z = F.mish(z)
+                elif op[0] == "leaky_relu":
+                    z = F.leaky_relu(z, op[1])
             return z
+
+        def unfused():
+            z = torch.mm(x, W.t())
+            z = eager_ops(z + bb, spec.ops)
+            if spec.reduction == "lse":
+                z = torch.logsumexp(z.float(), dim=1)
+            elif spec.reduction == "groupnorm":
+                z = F.group_norm(z, spec.gn_groups, g.to(tdt), be.to(tdt), spec.gn_eps)
+            return eager_ops(z, spec.post_ops)
 
         def gemm_only():
             return torch.mm(x, W.t())
@@ -221,7 +237,7 @@ def cpu_oracle_fgemm(spec, inp, budget_s, out, np):
         sel = slice(n_rows, n_rows + r)
         t0 = time.perf_counter()
         ref = ref_fgemm(x64[sel], W64, b, spec.ops, spec.reduction, spec.gn_groups, spec.gn_eps,
-                        inp.get("gamma"), inp.get("beta"))
+                        inp.get("gamma"), inp.get("beta"), spec.post_ops)
         t_total += time.perf_counter() - t0
         if first is None:
             first = (sel, ref)

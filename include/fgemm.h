@@ -10,10 +10,13 @@
  *     mixed-precision execution with fp32 accumulation and post-processing,
  *     single-pass reductions, partitioning without cross-block reductions).
  *     The tail is a chain of up to FG_MAX_OPS elementwise ops (scale, add,
- *     ReLU, GELU-tanh, SiLU, clamp — the pointwise vocabulary of Table III)
- *     optionally followed by one row reduction: LogSumExp over the N columns
- *     of each row, or GroupNorm over contiguous channel groups (Table III:
- *     Scale + LSE, Swish + GroupNorm).
+ *     ReLU, GELU-tanh, SiLU, clamp, Mish, LeakyReLU — the pointwise
+ *     vocabulary of Table III) optionally followed by one row reduction:
+ *     LogSumExp over the N columns of each row, or GroupNorm over contiguous
+ *     channel groups (Table III: Scale + LSE, Swish + GroupNorm), and then a
+ *     second chain of up to FG_MAX_OPS elementwise ops applied to the
+ *     reduction's result (Table III: LSE → Mish, GroupNorm → Swish → Mul →
+ *     Swish, GroupNorm → LeakyReLU → Sum).
  *
  *  2. moe_grouped_ffn: one MoE expert-FFN step of a gpt-oss-20b-like layer
  *     (paper §IV-A: the MoE decode path and its "MoE finalize" kernel,
@@ -66,7 +69,9 @@ typedef enum {
   FG_OP_RELU = 2,       /* max(z, 0) */
   FG_OP_GELU_TANH = 3,  /* ½z(1 + tanh(√(2/π)(z + 0.044715 z³))) */
   FG_OP_SILU = 4,       /* z/(1 + e^−z) */
-  FG_OP_CLAMP = 5       /* min(max(z, a), b); requires a ≤ b */
+  FG_OP_CLAMP = 5,      /* min(max(z, a), b); requires a ≤ b */
+  FG_OP_MISH = 6,       /* z·tanh(ln(1 + e^z))  (Mish, Table III) */
+  FG_OP_LEAKY_RELU = 7  /* z for z ≥ 0, a·z otherwise (LeakyReLU, Table III) */
 } fg_op_kind;
 
 typedef struct {
@@ -92,6 +97,10 @@ typedef struct {
   int32_t reduction;        /* fg_reduction */
   int32_t gn_groups;        /* GroupNorm only: N must be a multiple */
   float gn_eps;             /* GroupNorm only: ≥ 0 */
+  int32_t n_post_ops;       /* 0 .. FG_MAX_OPS; non-zero only with a reduction */
+  fg_op post_ops[FG_MAX_OPS]; /* applied in order to the reduction's result:
+                               per element after GroupNorm, per row value
+                               after LogSumExp */
 } fg_epilogue;
 
 typedef struct fg_plan fg_plan; /* opaque, host memory, immutable once built */

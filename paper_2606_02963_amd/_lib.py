@@ -17,7 +17,8 @@ LIB_PATH = os.path.join(_PKG, "libfgemm.so")
 FG_OK, FG_ERR_INVALID_ARG, FG_ERR_UNSUPPORTED, FG_ERR_ALIGNMENT, FG_ERR_WORKSPACE, FG_ERR_HIP = range(6)
 FG_F32, FG_BF16, FG_E4M3 = 0, 1, 2
 DTYPES = {"f32": FG_F32, "bf16": FG_BF16, "e4m3": FG_E4M3}
-OP_KINDS = {"scale": 0, "add": 1, "relu": 2, "gelu_tanh": 3, "silu": 4, "clamp": 5}
+OP_KINDS = {"scale": 0, "add": 1, "relu": 2, "gelu_tanh": 3, "silu": 4, "clamp": 5, "mish": 6,
+            "leaky_relu": 7}
 REDUCTIONS = {None: 0, "lse": 1, "groupnorm": 2}
 FG_MAX_OPS = 8
 
@@ -28,7 +29,8 @@ class FgOp(C.Structure):
 
 class FgEpilogue(C.Structure):
     _fields_ = [("has_bias", C.c_int32), ("n_ops", C.c_int32), ("ops", FgOp * FG_MAX_OPS),
-                ("reduction", C.c_int32), ("gn_groups", C.c_int32), ("gn_eps", C.c_float)]
+                ("reduction", C.c_int32), ("gn_groups", C.c_int32), ("gn_eps", C.c_float),
+                ("n_post_ops", C.c_int32), ("post_ops", FgOp * FG_MAX_OPS)]
 
 
 class MoeDesc(C.Structure):
@@ -98,21 +100,28 @@ def _check(st, func):
         raise FgError(st, func, last_error())
 
 
-def make_epilogue(has_bias=False, ops=(), reduction=None, gn_groups=0, gn_eps=1e-5):
-    """Build an FgEpilogue from ((kind, a, b), ...) tuples as used by the oracle."""
-    if len(ops) > FG_MAX_OPS:
-        raise ValueError(f"at most {FG_MAX_OPS} ops")
+def _fill_ops(dst, ops):
+    for i, op in enumerate(ops):
+        kind, a, b = (tuple(op) + (0.0, 0.0))[:3]
+        dst[i].kind = OP_KINDS[kind] if isinstance(kind, str) else int(kind)
+        dst[i].a = a
+        dst[i].b = b
+
+
+def make_epilogue(has_bias=False, ops=(), reduction=None, gn_groups=0, gn_eps=1e-5, post_ops=()):
+    """Build an FgEpilogue from ((kind, a, b), ...) tuples as used by the oracle.
+    post_ops are applied to the reduction's result."""
+    if len(ops) > FG_MAX_OPS or len(post_ops) > FG_MAX_OPS:
+        raise ValueError(f"at most {FG_MAX_OPS} ops per chain")
     e = FgEpilogue()
     e.has_bias = 1 if has_bias else 0
     e.n_ops = len(ops)
-    for i, op in enumerate(ops):
-        kind, a, b = (tuple(op) + (0.0, 0.0))[:3]
-        e.ops[i].kind = OP_KINDS[kind] if isinstance(kind, str) else int(kind)
-        e.ops[i].a = a
-        e.ops[i].b = b
+    _fill_ops(e.ops, ops)
     e.reduction = REDUCTIONS[reduction] if not isinstance(reduction, int) else reduction
     e.gn_groups = gn_groups
     e.gn_eps = gn_eps
+    e.n_post_ops = len(post_ops)
+    _fill_ops(e.post_ops, post_ops)
     return e
 
 

@@ -38,25 +38,29 @@ def _stream(stream):
     return s.cuda_stream
 
 
-def get_plan(M, N, K, in_dtype, out_dtype, has_bias, ops=(), reduction=None, gn_groups=0, gn_eps=1e-5):
+def get_plan(M, N, K, in_dtype, out_dtype, has_bias, ops=(), reduction=None, gn_groups=0, gn_eps=1e-5,
+             post_ops=()):
     """Cached fgemm plan for a problem description."""
     key = (M, N, K, in_dtype, out_dtype, bool(has_bias), tuple(tuple(o) for o in ops), reduction,
-           gn_groups, float(gn_eps))
+           gn_groups, float(gn_eps), tuple(tuple(o) for o in post_ops))
     p = _PLANS.get(key)
     if p is None:
-        epi = _lib.make_epilogue(has_bias, ops, reduction, gn_groups, gn_eps)
+        epi = _lib.make_epilogue(has_bias, ops, reduction, gn_groups, gn_eps, post_ops)
         p = _lib.fgemm_plan(M, N, K, in_dtype, out_dtype, epi)
         _PLANS[key] = p
     return p
 
 
 def linear_epilogue(x, W, bias=None, ops=(), reduction=None, gn_groups=0, gn_eps=1e-5,
-                    gamma=None, beta=None, out_dtype=None, out=None, workspace=None, stream=None):
+                    gamma=None, beta=None, out_dtype=None, out=None, workspace=None, stream=None,
+                    post_ops=()):
     """y = tail(x·Wᵀ + b) in one fused launch (two for a row LogSumExp).
 
     x [M, K] and W [N, K] (f32 or bf16, same dtype), bias/gamma/beta fp32 [N].
     ops: ((kind, a, b), ...) with kinds scale, add, relu, gelu_tanh, silu,
-    clamp. reduction: None, "lse" (returns fp32 [M]) or "groupnorm"."""
+    clamp, mish, leaky_relu. reduction: None, "lse" (returns fp32 [M]) or
+    "groupnorm". post_ops: ops of the same kinds applied to the reduction's
+    result."""
     M, K = x.shape
     N, K2 = W.shape
     if K2 != K or x.dtype != W.dtype:
@@ -64,7 +68,8 @@ def linear_epilogue(x, W, bias=None, ops=(), reduction=None, gn_groups=0, gn_eps
     in_dt = _dt_name(x)
     if out_dtype is None:
         out_dtype = "f32" if (in_dt == "f32" or reduction == "lse") else "bf16"
-    plan = get_plan(M, N, K, in_dt, out_dtype, bias is not None, ops, reduction, gn_groups, gn_eps)
+    plan = get_plan(M, N, K, in_dt, out_dtype, bias is not None, ops, reduction, gn_groups, gn_eps,
+                    post_ops)
     if out is None:
         shape = (M,) if reduction == "lse" else (M, N)
         out = torch.empty(shape, dtype=_TORCH_DT[out_dtype], device=x.device)

@@ -8,7 +8,9 @@
 // mean and variance come from the registers plus one exchange between the
 // two waves that share a row; LogSumExp spans N tiles, so each tile emits its
 // (max, Σexp) pair and a second, tiny pass combines them with the rescaling
-// identity of online softmax (§I).
+// identity of online softmax (§I). Table III also chains elementwise ops
+// after the reduction (LSE → Mish, GroupNorm → Swish → Mul → Swish); those
+// run on the normalised registers, or on the combined row value.
 #pragma once
 
 #include <math.h>
@@ -36,6 +38,33 @@ __device__ __forceinline__ float gelu_tanh(float u) {
 
 // SiLU u·σ(u); for u → −∞ it tends to −0.
 __device__ __forceinline__ float silu(float u) { return u * fast_sigmoid(u); }
+
+// Mish u·tanh(ln(1 + e^u)). With t = e^u, tanh(ln(1 + t)) = n/(n + 2) where
+// n = (1 + t)² − 1 = t(t + 2): one exponential and one reciprocal. Above
+// u = 20 the ratio is 1 in fp32, and clamping the exponent there keeps n
+// finite (n overflows near u = 44).
+__device__ __forceinline__ float mish(float u) {
+  const float t = fast_exp(fminf(u, 20.0f));
+  const float n = t * (t + 2.0f);
+  return u * (n * fast_rcp(n + 2.0f));
+}
+
+__device__ __forceinline__ float leaky_relu(float u, float slope) { return u >= 0.0f ? u : slope * u; }
+
+// One op on one value: the per-row values after a row LogSumExp.
+__device__ __forceinline__ float apply_op_scalar(int kind, float a, float b, float u) {
+  switch (kind) {
+    case FG_OP_SCALE: return u * a;
+    case FG_OP_ADD: return u + a;
+    case FG_OP_RELU: return fmaxf(u, 0.0f);
+    case FG_OP_GELU_TANH: return gelu_tanh(u);
+    case FG_OP_SILU: return silu(u);
+    case FG_OP_CLAMP: return fminf(fmaxf(u, a), b);
+    case FG_OP_MISH: return mish(u);
+    case FG_OP_LEAKY_RELU: return leaky_relu(u, a);
+    default: return u;
+  }
+}
 
 // The chain runs over one block of FN·4 accumulators at a time (one fm),
 // all ops on that block before the next, so only that block is live in
@@ -66,6 +95,8 @@ __device__ __forceinline__ void apply_ops(const EpiArgs& ep, f32x4 (&acc)[TL::FM
         case FG_OP_GELU_TANH: FG_EACH(gelu_tanh(u)) break;
         case FG_OP_SILU: FG_EACH(silu(u)) break;
         case FG_OP_CLAMP: FG_EACH(fminf(fmaxf(u, a), b)) break;
+        case FG_OP_MISH: FG_EACH(mish(u)) break;
+        case FG_OP_LEAKY_RELU: FG_EACH(leaky_relu(u, a)) break;
         default: break;
       }
 #undef FG_EACH

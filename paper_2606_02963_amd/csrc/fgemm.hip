@@ -142,7 +142,7 @@ __device__ __forceinline__ bool split_k_gather(const DenseArgs& a, int tile, int
 }
 
 template <class TL, int RED, int OUT>
-__global__ __launch_bounds__(TL::THREADS) void fgemm_kernel(DenseArgs a, EpiArgs ep) {
+__global__ __launch_bounds__(TL::THREADS) void fgemm_kernel(DenseArgs a, EpiArgs ep, EpiArgs post) {
   __shared__ __attribute__((aligned(16))) char lds[DenseLds<TL>::BYTES];
   const int t = xcd_order(blockIdx.x, a.tiles_m * a.tiles_n * a.ks);
   const int ks = t % a.ks, tile = t / a.ks;
@@ -169,8 +169,10 @@ __global__ __launch_bounds__(TL::THREADS) void fgemm_kernel(DenseArgs a, EpiArgs
     lse_partials<TL>(acc, red, m0, n0, a.M, a.N, tn, a.tiles_n, a.ws);
     return;
   }
-  if constexpr (RED == FG_RED_GROUPNORM)
+  if constexpr (RED == FG_RED_GROUPNORM) {
     groupnorm_tile<TL>(acc, red, n0, a.N, a.gn_width, a.gn_eps, a.gamma, a.beta);
+    apply_ops<TL>(post, acc);
+  }
 
   if constexpr (OUT == OUT_BF16) {
     char* out = reinterpret_cast<char*>(a.out);
@@ -203,8 +205,10 @@ __global__ __launch_bounds__(TL::THREADS) void fgemm_kernel(DenseArgs a, EpiArgs
   }
 }
 
-// out[m] = max_j m_j + log Σ_j s_j·exp(m_j − max_j m_j); one wave per row.
-__global__ __launch_bounds__(256) void lse_combine_kernel(const float2* ws, float* out, int M, int tiles_n) {
+// out[m] = post(max_j m_j + log Σ_j s_j·exp(m_j − max_j m_j)); one wave per
+// row.
+__global__ __launch_bounds__(256) void lse_combine_kernel(const float2* ws, float* out, int M, int tiles_n,
+                                                          EpiArgs post) {
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int l = threadIdx.x & 63;
   if (row >= M) return;
@@ -217,7 +221,11 @@ __global__ __launch_bounds__(256) void lse_combine_kernel(const float2* ws, floa
   for (int j = l; j < tiles_n; j += 64) s += p[j].y * expf(p[j].x - mx);
 #pragma unroll
   for (int m = 1; m < 64; m <<= 1) s += __shfl_xor(s, m, 64);
-  if (l == 0) out[row] = mx + logf(s);
+  if (l == 0) {
+    float v = mx + logf(s);
+    for (int o = 0; o < post.n_ops; ++o) v = apply_op_scalar(post.kind[o], post.a[o], post.b[o], v);
+    out[row] = v;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -242,7 +250,7 @@ static const TileModel kBf16Tiles[] = {
     {CFG_BF16_128x128, 128, 128, 0.72},
 };
 
-typedef void (*KernelFn)(DenseArgs, EpiArgs);
+typedef void (*KernelFn)(DenseArgs, EpiArgs, EpiArgs);
 
 struct KernelChoice {
   KernelFn fn;
@@ -313,20 +321,29 @@ extern "C" fg_status fgemm_plan(fg_plan** plan, int64_t M, int64_t N, int64_t K,
     return fail(FG_ERR_INVALID_ARG, "fgemm_plan: output dtype %d not supported (f32 or bf16)", out_dtype);
   if (epi->n_ops < 0 || epi->n_ops > FG_MAX_OPS)
     return fail(FG_ERR_INVALID_ARG, "fgemm_plan: n_ops=%d outside 0..%d", epi->n_ops, FG_MAX_OPS);
-  for (int i = 0; i < epi->n_ops; ++i) {
-    const fg_op& op = epi->ops[i];
-    if (op.kind < FG_OP_SCALE || op.kind > FG_OP_CLAMP)
-      return fail(FG_ERR_INVALID_ARG, "fgemm_plan: op %d has unknown kind %d", i, op.kind);
-    if (op.kind == FG_OP_CLAMP && !(op.a <= op.b))
-      return fail(FG_ERR_INVALID_ARG, "fgemm_plan: clamp op %d needs lo <= hi", i);
-    if (!isfinite(op.a) || !isfinite(op.b))
-      return fail(FG_ERR_INVALID_ARG, "fgemm_plan: op %d has a non-finite parameter", i);
+  if (epi->n_post_ops < 0 || epi->n_post_ops > FG_MAX_OPS)
+    return fail(FG_ERR_INVALID_ARG, "fgemm_plan: n_post_ops=%d outside 0..%d", epi->n_post_ops, FG_MAX_OPS);
+  for (int chain = 0; chain < 2; ++chain) {
+    const fg_op* ops = chain == 0 ? epi->ops : epi->post_ops;
+    const int n = chain == 0 ? epi->n_ops : epi->n_post_ops;
+    const char* what = chain == 0 ? "op" : "post op";
+    for (int i = 0; i < n; ++i) {
+      const fg_op& op = ops[i];
+      if (op.kind < FG_OP_SCALE || op.kind > FG_OP_LEAKY_RELU)
+        return fail(FG_ERR_INVALID_ARG, "fgemm_plan: %s %d has unknown kind %d", what, i, op.kind);
+      if (op.kind == FG_OP_CLAMP && !(op.a <= op.b))
+        return fail(FG_ERR_INVALID_ARG, "fgemm_plan: clamp %s %d needs lo <= hi", what, i);
+      if (!isfinite(op.a) || !isfinite(op.b))
+        return fail(FG_ERR_INVALID_ARG, "fgemm_plan: %s %d has a non-finite parameter", what, i);
+    }
   }
   if (epi->has_bias != 0 && epi->has_bias != 1)
     return fail(FG_ERR_INVALID_ARG, "fgemm_plan: has_bias must be 0 or 1");
   const int red = epi->reduction;
   if (red != FG_RED_NONE && red != FG_RED_LOGSUMEXP_ROW && red != FG_RED_GROUPNORM)
     return fail(FG_ERR_INVALID_ARG, "fgemm_plan: unknown reduction %d", red);
+  if (red == FG_RED_NONE && epi->n_post_ops != 0)
+    return fail(FG_ERR_INVALID_ARG, "fgemm_plan: post ops need a reduction (append them to ops instead)");
   if (red == FG_RED_LOGSUMEXP_ROW && out_dtype != FG_F32)
     return fail(FG_ERR_INVALID_ARG, "fgemm_plan: LogSumExp output must be f32");
   const int epc = in_dtype == FG_F32 ? 4 : 8;
@@ -472,13 +489,20 @@ extern "C" fg_status fgemm_run(const fg_plan* plan, const void* A, const void* W
   a.partials = p.ks > 1 ? reinterpret_cast<f32x4*>(static_cast<char*>(workspace) + p.part_off) : nullptr;
   a.gn_width = red == FG_RED_GROUPNORM ? (int)(p.N / p.epi.gn_groups) : 0;
   a.gn_eps = p.epi.gn_eps;
-  EpiArgs ep;
+  EpiArgs ep, post;
   memset(&ep, 0, sizeof(ep));
+  memset(&post, 0, sizeof(post));
   ep.n_ops = p.epi.n_ops;
   for (int i = 0; i < p.epi.n_ops; ++i) {
     ep.kind[i] = p.epi.ops[i].kind;
     ep.a[i] = p.epi.ops[i].a;
     ep.b[i] = p.epi.ops[i].b;
+  }
+  post.n_ops = p.epi.n_post_ops;
+  for (int i = 0; i < p.epi.n_post_ops; ++i) {
+    post.kind[i] = p.epi.post_ops[i].kind;
+    post.a[i] = p.epi.post_ops[i].a;
+    post.b[i] = p.epi.post_ops[i].b;
   }
   const int out_k = p.out_dt == FG_BF16 ? OUT_BF16 : OUT_F32;
   KernelChoice kc{nullptr, 0};
@@ -491,11 +515,11 @@ extern "C" fg_status fgemm_run(const fg_plan* plan, const void* A, const void* W
   if (kc.fn == nullptr) return fail(FG_ERR_UNSUPPORTED, "fgemm_run: no kernel for this plan");
   hipStream_t s = static_cast<hipStream_t>(stream);
   const unsigned grid = (unsigned)(p.tiles_m * p.tiles_n * p.ks);
-  hipLaunchKernelGGL(kc.fn, dim3(grid), dim3(kc.threads), 0, s, a, ep);
+  hipLaunchKernelGGL(kc.fn, dim3(grid), dim3(kc.threads), 0, s, a, ep, post);
   if (red == FG_RED_LOGSUMEXP_ROW) {
     const unsigned g2 = (unsigned)((p.M + 3) / 4);
     hipLaunchKernelGGL(lse_combine_kernel, dim3(g2), dim3(256), 0, s, a.ws, static_cast<float*>(out),
-                       (int)p.M, (int)p.tiles_n);
+                       (int)p.M, (int)p.tiles_n, post);
   }
   return check_launch("fgemm_run");
 }

@@ -74,6 +74,7 @@ class FgemmSpec:
     gn_groups: int = 0
     gn_eps: float = 1e-5
     out_dtype: str = None         # default: f32 for f32/LSE, else bf16
+    post_ops: tuple = ()          # ops applied to the reduction's result
 
     @property
     def out(self):
@@ -103,7 +104,7 @@ class FgemmSpec:
         return FgemmSpec(name or f"{self.name}@{M or self.M}x{N2}x{K or self.K}",
                          M or self.M, N2, K or self.K, self.dtype,
                          self.w_bound, self.ops, self.reduction, groups,
-                         self.gn_eps, self.out_dtype)
+                         self.gn_eps, self.out_dtype, self.post_ops)
 
 
 FGEMM_SPECS = {
@@ -120,6 +121,21 @@ FGEMM_SPECS = {
     # GroupNorm(32 × 128, eps 1e-5)(SiLU(x·Wᵀ + b)); γ ~ U(0.5,1.5), β ~ N(0,0.1)
     "bf16_silu_gn": FgemmSpec("bf16_silu_gn", 2048, 4096, 4096, "bf16", 1 / 64,
                               (("silu",),), "groupnorm", 32, 1e-5),
+    # The four tail chains of paper Table III. Their problem shapes are not
+    # in the paper; they take the shapes of the LSE and GroupNorm workloads
+    # above. "Mul" is read as a scalar multiply, "Sum" as adding a constant
+    # (Swish → Sum → GN) or the tensor to itself, x + x = 2x (GN → LReLU →
+    # Sum); the LeakyReLU slope is 0.01.
+    "bf16_scale_lse_mish": FgemmSpec("bf16_scale_lse_mish", 4096, 8192, 4096, "bf16", 1 / 64,
+                                     (("scale", 2.0),), "lse", post_ops=(("mish",),)),
+    "bf16_gn_swish_mul_swish": FgemmSpec("bf16_gn_swish_mul_swish", 2048, 4096, 4096, "bf16", 1 / 64,
+                                         (), "groupnorm", 32, 1e-5,
+                                         post_ops=(("silu",), ("scale", 1.5), ("silu",))),
+    "bf16_gn_lrelu_sum": FgemmSpec("bf16_gn_lrelu_sum", 2048, 4096, 4096, "bf16", 1 / 64,
+                                   (), "groupnorm", 32, 1e-5,
+                                   post_ops=(("leaky_relu", 0.01), ("scale", 2.0))),
+    "bf16_swish_sum_gn": FgemmSpec("bf16_swish_sum_gn", 2048, 4096, 4096, "bf16", 1 / 64,
+                                   (("silu",), ("add", 0.25)), "groupnorm", 32, 1e-5),
 }
 
 

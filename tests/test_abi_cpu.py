@@ -85,6 +85,28 @@ def test_plan_validation_statuses():
     assert plan_status(8, 4096, 256, "bf16", "bf16", gn_neg) == L.FG_ERR_INVALID_ARG
 
 
+def test_post_op_validation():
+    gn = dict(reduction="groupnorm", gn_groups=32, gn_eps=1e-5)
+    chain = (("silu",), ("scale", 1.5), ("mish",), ("leaky_relu", 0.01))
+    assert plan_status(8, 4096, 256, "bf16", "bf16", E(post_ops=chain, **gn)) == L.FG_OK
+    assert plan_status(8, 100, 256, "bf16", "f32", E(reduction="lse", post_ops=chain)) == L.FG_OK
+    assert plan_status(8, 256, 256, "bf16", "bf16", E(ops=chain)) == L.FG_OK     # new kinds as ops
+    # post ops without a reduction are rejected: they would be ordinary ops
+    assert plan_status(8, 256, 256, "bf16", "bf16", E(post_ops=(("relu",),))) == L.FG_ERR_INVALID_ARG
+    assert plan_status(8, 4096, 256, "bf16", "bf16", E(post_ops=((8, 0.0),), **gn)) == L.FG_ERR_INVALID_ARG
+    assert plan_status(8, 4096, 256, "bf16", "bf16",
+                       E(post_ops=(("clamp", 2.0, 1.0),), **gn)) == L.FG_ERR_INVALID_ARG
+    assert plan_status(8, 4096, 256, "bf16", "bf16",
+                       E(post_ops=(("leaky_relu", float("inf")),), **gn)) == L.FG_ERR_INVALID_ARG
+    for n in (-1, 9):
+        e = E(post_ops=(("relu",),), **gn)
+        e.n_post_ops = n
+        assert plan_status(8, 4096, 256, "bf16", "bf16", e) == L.FG_ERR_INVALID_ARG
+    with pytest.raises(L.FgError):
+        L.fgemm_plan(8, 256, 256, "bf16", "bf16", E(post_ops=(("relu",),)))
+    assert "post op" in L.last_error()
+
+
 def test_last_error_describes_the_failure():
     with pytest.raises(L.FgError) as ei:
         L.fgemm_plan(8, 256, 260, "bf16", "bf16", E())

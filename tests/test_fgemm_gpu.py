@@ -40,13 +40,13 @@ def run_spec(spec, seed=0, rows=None, inp=None, with_bias=True):
     inp = inp if inp is not None else make_fgemm_inputs(spec, seed)
     (x, W, b, g, be), (x64, W64) = _device_inputs(spec, inp)
     y = api.linear_epilogue(x, W, b if with_bias else None, spec.ops, spec.reduction, spec.gn_groups,
-                            spec.gn_eps, g, be, out_dtype=spec.out)
+                            spec.gn_eps, g, be, out_dtype=spec.out, post_ops=spec.post_ops)
     torch.cuda.synchronize()
     got = host64(y)
     sel = slice(None) if rows is None else np.asarray(rows)
     ref = ref_fgemm(x64[sel], W64, inp["b"].astype(np.float64) if with_bias else None, spec.ops,
                     spec.reduction, spec.gn_groups, spec.gn_eps,
-                    inp.get("gamma"), inp.get("beta"))
+                    inp.get("gamma"), inp.get("beta"), spec.post_ops)
     rep = compare(got[sel], ref, "f32" if spec.dtype == "f32" else "bf16")
     log(f"    {rep}")
     assert rep.ok, f"{spec.name}: {rep}"
@@ -85,6 +85,42 @@ SMALL = [
 @pytest.mark.parametrize("spec", SMALL, ids=lambda s: s.name)
 def test_parity_small(spec):
     run_spec(spec)
+
+
+# Table III tail chains: Mish, LeakyReLU and elementwise ops after the
+# reduction, on every tile configuration and after a split-K gather.
+T3 = [FGEMM_SPECS[k] for k in ("bf16_scale_lse_mish", "bf16_gn_swish_mul_swish", "bf16_gn_lrelu_sum",
+                               "bf16_swish_sum_gn")]
+TABLE3 = []
+for _s in T3:
+    TABLE3 += [
+        _s.scaled(M=300, N=512, K=264),        # 128×128 tiles, ragged M, K tail
+        _s.scaled(M=2048, N=4096, K=128),      # 256×128 tiles
+        _s.scaled(M=4000, N=4096, K=200),      # 256×256 tiles, ragged M
+        _s.scaled(M=1000, N=2048, K=4104),     # split-K gather, K tail
+    ]
+TABLE3 += [
+    # the LSE chain with a ragged N inside the last tile
+    T3[0].scaled(M=300, N=1000, K=264),
+    # Mish and LeakyReLU as ordinary ops before a plain store, and large
+    # arguments (weights ×16 push |z| past Mish's exponent clamp at 20)
+    FgemmSpec("bf16_mish_lrelu", 130, 264, 200, "bf16", 0.1, (("mish",), ("leaky_relu", 0.2))),
+    FgemmSpec("bf16_mish_large", 130, 264, 512, "bf16", 1.6, (("mish",),)),
+    FgemmSpec("f32_lse_mish", 96, 256, 64, "f32", 0.2, (("scale", 2.0),), "lse", post_ops=(("mish",),)),
+    FgemmSpec("f32_gn_lrelu", 96, 256, 64, "f32", 0.2, (), "groupnorm", 2, 1e-5,
+              post_ops=(("leaky_relu", 0.01), ("scale", 2.0))),
+]
+
+
+@pytest.mark.parametrize("spec", TABLE3, ids=lambda s: s.name)
+def test_parity_table3_chains(spec):
+    run_spec(spec)
+
+
+@pytest.mark.parametrize("spec", T3, ids=lambda s: s.name)
+def test_parity_table3_full_size_sampled_rows(spec):
+    rows = [0, 1, 255, 256, spec.M // 2 + 3, spec.M - 1]
+    run_spec(spec, rows=rows)
 
 
 @pytest.mark.parametrize("spec", [C2, C3, C4], ids=lambda s: s.name)
