@@ -15,7 +15,9 @@ y = tail(x·Wᵀ + b), here evaluated in fp64 on the exact values the GPU reads.
 The MoE expert FFN (paper §IV-A, the gpt-oss-20b decode path: MoE finalize,
 and the MoE-MLP block named as future work in §V) is written out step by step
 in the order routing → permutation → grouped gate/up GEMM → clamped SwiGLU →
-grouped down GEMM → routing-weighted finalize.
+grouped down GEMM → routing-weighted finalize. The other two decode kernels
+of Table I are here too: the fused residual add + RMSNorm (``norm``) and the
+QKV bias + rotary embedding + KV-cache update (``rope``).
 
 Every function is pinned by tests in ``tests/test_oracle_*.py`` against closed
 forms, invariants, brute force (mpmath) and library special cases; none is
@@ -27,11 +29,13 @@ from .codecs import (bf16_decode, bf16_encode_rne, e4m3_decode,
 from .fgemm import ref_fgemm, OPS
 from .moe import ref_route, ref_permute, ref_swiglu_clamped, ref_moe, ref_moe_finalize, ref_quant_rows_e4m3
 from .norm import ref_add_rmsnorm
+from .rope import ref_rope, ref_bias_rope_kv_update
 from .compare import rel_err, ComparisonReport, compare
 
 __all__ = [
     "bf16_decode", "bf16_encode_rne", "e4m3_decode", "e4m3_encode_rne_sat",
     "f32_round", "ref_fgemm", "OPS", "ref_route", "ref_permute",
-    "ref_swiglu_clamped", "ref_moe", "ref_moe_finalize", "ref_quant_rows_e4m3", "ref_add_rmsnorm", "rel_err",
+    "ref_swiglu_clamped", "ref_moe", "ref_moe_finalize", "ref_quant_rows_e4m3", "ref_add_rmsnorm",
+    "ref_rope", "ref_bias_rope_kv_update", "rel_err",
     "ComparisonReport", "compare",
 ]

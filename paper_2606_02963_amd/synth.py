@@ -270,3 +270,60 @@ def make_norm_inputs(T, H=NORM_H, seed=0):
     r = to_bf16_bits(_normal(rng, (T, H), 4.0))
     w = to_bf16_bits((rng.random(H, dtype=np.float32) + np.float32(0.5)).astype(np.float32))
     return x, r, w
+
+
+# --------------------------------------------------------------------------
+# QKV bias + rotary embedding + KV-cache update (paper §IV-A, Table I): the
+# same batch sizes. The attention geometry is not in the paper; these are
+# gpt-oss-20b's published attention sizes (64 query heads and 8 key/value
+# heads of 64 values, rotary base 150000), with a paged cache of 64-token
+# blocks.
+
+@dataclass(frozen=True)
+class RopeSpec:
+    T: int
+    n_q: int = 64
+    n_kv: int = 8
+    D: int = 64
+    block_size: int = 64
+    base: float = 150000.0
+    interleaved: bool = False
+    max_pos: int = 8192            # positions ~ U{0 .. max_pos − 1}
+
+    @property
+    def width(self):
+        return (self.n_q + 2 * self.n_kv) * self.D
+
+    @property
+    def max_blocks(self):
+        return (self.max_pos + self.block_size - 1) // self.block_size
+
+    @property
+    def num_blocks(self):
+        return 2 * self.T + 16
+
+    def bytes(self):
+        """Algorithmic bytes of one step: qkv and bias read, q and the new K/V
+        cache rows written (bf16), positions and the used block-table entries
+        read."""
+        return (self.T * self.width + self.width + self.T * self.n_q * self.D
+                + 2 * self.T * self.n_kv * self.D) * 2 + self.T * 8
+
+
+def make_rope_inputs(spec, seed=0):
+    """qkv [T, width] ~ N(0, 1) and bias [width] ~ U(−0.1, 0.1) as bf16 bits,
+    positions [T] int32 ~ U{0 .. max_pos − 1}, block_table [T, max_blocks]
+    int32 and the cache's prior contents [num_blocks, 2, n_kv, block_size, D]
+    ~ N(0, 1) bf16 bits. Each token's current block is a distinct block id;
+    the other table entries hold ids of blocks no token of the step writes,
+    so a wrong table lookup lands in a block that must stay unchanged."""
+    rng = np.random.default_rng([seed, 4000 + spec.T])
+    qkv = to_bf16_bits(_normal(rng, (spec.T, spec.width), 1.0))
+    bias = to_bf16_bits(_uniform(rng, (spec.width,), 0.1))
+    pos = rng.integers(0, spec.max_pos, spec.T).astype(np.int32)
+    perm = rng.permutation(spec.num_blocks).astype(np.int32)
+    current, others = perm[:spec.T], perm[spec.T:]
+    table = others[rng.integers(0, others.size, (spec.T, spec.max_blocks))].astype(np.int32)
+    table[np.arange(spec.T), pos // spec.block_size] = current
+    cache = to_bf16_bits(_normal(rng, (spec.num_blocks, 2, spec.n_kv, spec.block_size, spec.D), 1.0))
+    return {"qkv": qkv, "bias": bias, "positions": pos, "block_table": table, "cache": cache}
