@@ -14,7 +14,7 @@ it, and the fp64 CPU oracle timed on a bounded sample of rows.
 Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
                        [--workload gelu_clamp|lse|silu_gn|tiny_f32|scale_lse_mish|gn_swish_mul_swish|
                                    gn_lrelu_sum|swish_sum_gn|moe_{prefill,decode}_{bf16,e4m3}|
-                                   moe_finalize|add_rmsnorm]
+                                   moe_finalize|add_rmsnorm|rope_kv]
 """
 
 import argparse
@@ -50,7 +50,8 @@ def parse():
     ap.add_argument("--workload", default="gelu_clamp",
                     choices=["gelu_clamp", "lse", "silu_gn", "tiny_f32", "scale_lse_mish",
                              "gn_swish_mul_swish", "gn_lrelu_sum", "swish_sum_gn", "moe_prefill_bf16",
-                             "moe_prefill_e4m3", "moe_decode_bf16", "moe_decode_e4m3", "moe_finalize", "add_rmsnorm"],
+                             "moe_prefill_e4m3", "moe_decode_bf16", "moe_decode_e4m3", "moe_finalize", "add_rmsnorm",
+                             "rope_kv"],
                     help="gelu_clamp (default) is the headline workload; the others are the "
                          "remaining configurations, measured the same way")
     return ap.parse_args()
@@ -456,6 +457,81 @@ def bench_add_rmsnorm(args, torch, np):
     return result
 
 
+def bench_rope_kv(args, torch, np):
+    """QKV bias + RoPE + paged KV-cache update over the batch sizes of paper
+    Table I (gpt-oss-20b attention sizes: 64 query and 8 key/value heads of
+    64, base 150000, 64-token blocks), timed like the finalize: launches
+    captured back to back in one HIP graph. Every launch rewrites the same
+    cache rows with the same values. The headline line is T = 128."""
+    from paper_2606_02963_amd import api
+    from paper_2606_02963_amd.synth import FINALIZE_BATCHES, RopeSpec, make_rope_inputs
+
+    reps = 50
+    dev = torch.device("cuda", 0)
+    bf = lambda a: torch.from_numpy(np.ascontiguousarray(a).view(np.int16)).view(torch.bfloat16).to(dev)  # noqa: E731
+    sweep = {}
+    for T in FINALIZE_BATCHES:
+        spec = RopeSpec(T)
+        inp = make_rope_inputs(spec)
+        qkv, bias, cache = bf(inp["qkv"]), bf(inp["bias"]), bf(inp["cache"])
+        pos = torch.from_numpy(inp["positions"]).to(dev)
+        table = torch.from_numpy(inp["block_table"]).to(dev)
+        q = torch.empty((T, spec.n_q, spec.D), dtype=torch.bfloat16, device=dev)
+
+        def step():
+            api.bias_rope_kv_update(qkv, bias, pos, table, cache, spec.n_q, spec.n_kv, spec.D, spec.base,
+                                    q_out=q)
+
+        step()
+        torch.cuda.synchronize()
+        eager_q, eager_c = q.clone(), cache.clone()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                step()
+        g.replay()
+        torch.cuda.synchronize()
+        if not (torch.equal(q, eager_q) and torch.equal(cache, eager_c)):
+            raise RuntimeError("graph replay of bias_rope_kv_update differs from the eager launch")
+        settle(g.replay, min(args.warmup_seconds, 0.3), torch)
+        ms = time_steps(g.replay, max(args.steps // 5, 5), max(args.warmup // 5, 2), torch) / reps
+        nbytes = spec.bytes()
+        sweep[T] = {"us": round(ms * 1e3, 3), "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1), "bytes": nbytes}
+    T = FINALIZE_BATCHES[-1]
+    spec = RopeSpec(T)
+    head = sweep[T]
+    roof = {"bound": "hbm", "achieved": head["gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+            "frac": round(head["gbs"] / PEAK_HBM_GBS, 4), "traffic": None,
+            "algorithmic_bytes_per_launch": head["bytes"]}
+    result = {
+        "metric": "bias + RoPE + KV-cache update effective HBM GB/s (paper Table I batch sweep)",
+        "value": head["gbs"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(head["us"] / 1e3, 6), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded: qkv ~ N(0,1), bias ~ U(-0.1,0.1), positions ~ U{0..8191}; see "
+                "paper_2606_02963_amd/synth.py)",
+        "config": {"workload": f"QKV bias + RoPE + paged KV write, qkv[{T}, {spec.width}] bf16, "
+                               f"{spec.n_q} q / {spec.n_kv} kv heads x {spec.D}, base {spec.base:g}, "
+                               f"{spec.block_size}-token blocks",
+                   "T": T, "launches_per_graph": reps},
+        "roofline": roof, "sweep": {str(t): v for t, v in sweep.items()}}
+    if not args.no_cpu_baseline:
+        from oracle import bf16_decode, ref_bias_rope_kv_update
+        inp = make_rope_inputs(spec)
+        args64 = (bf16_decode(inp["qkv"]), bf16_decode(inp["bias"]), inp["positions"], inp["block_table"],
+                  bf16_decode(inp["cache"]), spec.n_q, spec.n_kv, spec.D, spec.block_size, spec.base)
+        t0, n = time.perf_counter(), 0
+        while time.perf_counter() - t0 < 1.0:
+            ref_bias_rope_kv_update(*args64)
+            n += 1
+        sec = (time.perf_counter() - t0) / n
+        result["cpu_baseline"] = {"value": round(head["bytes"] / sec / 1e9, 3), "unit": "GB/s",
+                                  "cores": 1, "kind": "oracle",
+                                  "sample": f"the whole T={T} step, {n} repetitions in ~1 s",
+                                  "seconds": round(sec, 6)}
+    return result
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -480,6 +556,8 @@ def main():
         result = bench_finalize(args, torch, np)
     elif args.workload == "add_rmsnorm":
         result = bench_add_rmsnorm(args, torch, np)
+    elif args.workload == "rope_kv":
+        result = bench_rope_kv(args, torch, np)
     else:
         result = bench_fgemm(args, torch, np)
     if args.copy_calibration_mb > 0:

@@ -240,6 +240,54 @@ fg_status add_rmsnorm(const void *x, void *residual, const void *weight,
                       void *out, int64_t T, int64_t H, float eps, void *stream);
 
 /*
+ * bias_rope_kv_update — QKV bias + rotary position embedding + paged KV-cache
+ * write of one decode step (paper §IV-A, "Bias + RoPE + KV update" in
+ * Table I). Each of the T tokens is the newest token of its own sequence, at
+ * position positions[t]:
+ *   s = qkv[t] + bias (fp32), split into n_q_heads query, n_kv_heads key and
+ *   n_kv_heads value heads of head_dim values, in that order;
+ *   query and key heads are rotated (RoFormer's rotary embedding): pair i of
+ *   a head, (a, b), becomes (a·cos φ − b·sin φ, a·sin φ + b·cos φ) with
+ *   φ = pos·rope_base^(−2i/head_dim); pairs are (i, i + head_dim/2) or, with
+ *   `interleaved`, (2i, 2i + 1). The angle and its sine and cosine are taken
+ *   in fp64, the rotation in fp32;
+ *   q_out[t, h, :] = bf16(rotated query head h);
+ *   kv_cache[blk, 0, h, r, :] = bf16(rotated key head h) and
+ *   kv_cache[blk, 1, h, r, :] = bf16(value head h), with
+ *   blk = block_table[t·max_blocks + pos / block_size], r = pos % block_size.
+ * A token whose position is negative or at least max_blocks·block_size, or
+ * whose block id lies outside [0, num_blocks), writes nothing to the cache
+ * (its q_out row is still written). Two tokens of one call must not map to
+ * the same cache row (their writes would race).
+ *   qkv          [T, (n_q_heads + 2·n_kv_heads)·head_dim] bf16.
+ *   bias         [(n_q_heads + 2·n_kv_heads)·head_dim] bf16, or NULL (no bias).
+ *   positions    [T] int32.   block_table [T, max_blocks] int32.
+ *   q_out        [T, n_q_heads, head_dim] bf16; must not overlap qkv.
+ *   kv_cache     [num_blocks, 2, n_kv_heads, block_size, head_dim] bf16, read
+ *                nowhere, written only in the rows above.
+ * All caller-owned device memory; bf16 pointers 16-byte aligned, int32
+ * pointers 4-byte aligned. FG_ERR_INVALID_ARG for a NULL desc or pointer
+ * (bias excepted), bad sizes or a non-finite / non-positive base;
+ * FG_ERR_ALIGNMENT for misaligned pointers or head_dim not a multiple of 16;
+ * FG_ERR_UNSUPPORTED for head_dim above 256. T = 0 enqueues nothing.
+ */
+typedef struct {
+  int64_t T;                /* decode tokens (one per sequence), 0 .. 2^31 − 1 */
+  int32_t n_q_heads;        /* ≥ 1 */
+  int32_t n_kv_heads;       /* ≥ 1 */
+  int32_t head_dim;         /* multiple of 16, 16 .. 256 */
+  int32_t block_size;       /* tokens per cache block, ≥ 1 */
+  int32_t max_blocks;       /* entries per block_table row, ≥ 1 */
+  int64_t num_blocks;       /* blocks in kv_cache, ≥ 1 */
+  float rope_base;          /* θ base, finite and > 0 (gpt-oss: 150000) */
+  int32_t interleaved;      /* 0: pairs (i, i + head_dim/2); 1: (2i, 2i + 1) */
+} rope_desc;
+
+fg_status bias_rope_kv_update(const rope_desc *d, const void *qkv, const void *bias,
+                              const int32_t *positions, const int32_t *block_table,
+                              void *q_out, void *kv_cache, void *stream);
+
+/*
  * fg_quantize_rows_e4m3 — the W8A8 path's activation quantiser as a
  * standalone call: for each of `rows` rows of `cols` bf16 values,
  * s = amax/448 (1 for an all-zero row) and q = e4m3fn(v/s) with

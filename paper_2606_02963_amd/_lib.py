@@ -39,6 +39,12 @@ class MoeDesc(C.Structure):
                 ("swiglu_limit", C.c_float), ("gateup_interleaved", C.c_int32)]
 
 
+class RopeDesc(C.Structure):
+    _fields_ = [("T", C.c_int64), ("n_q_heads", C.c_int32), ("n_kv_heads", C.c_int32),
+                ("head_dim", C.c_int32), ("block_size", C.c_int32), ("max_blocks", C.c_int32),
+                ("num_blocks", C.c_int64), ("rope_base", C.c_float), ("interleaved", C.c_int32)]
+
+
 class FgError(RuntimeError):
     def __init__(self, status, func, detail):
         self.status = status
@@ -77,6 +83,8 @@ def lib():
         L.moe_finalize.restype = i32
         L.add_rmsnorm.argtypes = [vp, vp, vp, vp, i64, i64, C.c_float, vp]
         L.add_rmsnorm.restype = i32
+        L.bias_rope_kv_update.argtypes = [C.POINTER(RopeDesc), vp, vp, vp, vp, vp, vp, vp]
+        L.bias_rope_kv_update.restype = i32
         L.fg_quantize_rows_e4m3.argtypes = [vp, i64, i64, vp, vp, vp]
         L.fg_quantize_rows_e4m3.restype = i32
         L.fg_status_str.argtypes = [i32]
@@ -209,3 +217,18 @@ def moe_finalize(y_slot, out, T, H, top_k, stream=None):
 def add_rmsnorm(x, residual, weight, out, T, H, eps, stream=None):
     """residual <- bf16(x + residual); out = bf16(RMSNorm(x + residual) * weight)."""
     _check(lib().add_rmsnorm(x, residual, weight, out, T, H, eps, stream), "add_rmsnorm")
+
+
+def rope_desc(T, n_q, n_kv, D, block_size, max_blocks, num_blocks, base, interleaved=False):
+    d = RopeDesc()
+    d.T, d.n_q_heads, d.n_kv_heads, d.head_dim = int(T), int(n_q), int(n_kv), int(D)
+    d.block_size, d.max_blocks, d.num_blocks = int(block_size), int(max_blocks), int(num_blocks)
+    d.rope_base = base
+    d.interleaved = 1 if interleaved else 0
+    return d
+
+
+def bias_rope_kv_update(desc, qkv, bias, positions, block_table, q_out, kv_cache, stream=None):
+    """q_out = RoPE(q + b); kv_cache rows at each token's position = (RoPE(k + b), v + b)."""
+    _check(lib().bias_rope_kv_update(C.byref(desc) if desc is not None else None, qkv, bias, positions,
+                                     block_table, q_out, kv_cache, stream), "bias_rope_kv_update")

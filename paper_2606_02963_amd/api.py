@@ -153,3 +153,32 @@ def add_rmsnorm(x, residual, weight, eps=1e-5, out=None, stream=None):
     _lib.add_rmsnorm(_dev(x, "x"), _dev(residual, "residual"), _dev(weight, "weight"), _dev(out, "out"),
                      T, H, eps, _stream(stream))
     return out
+
+
+def bias_rope_kv_update(qkv, bias, positions, block_table, kv_cache, n_q, n_kv, head_dim, rope_base,
+                        interleaved=False, q_out=None, stream=None):
+    """QKV bias + rotary embedding + paged KV-cache write of one decode step.
+
+    qkv [T, (n_q + 2·n_kv)·head_dim] bf16, bias [(n_q + 2·n_kv)·head_dim] bf16
+    or None, positions [T] int32, block_table [T, max_blocks] int32, kv_cache
+    [num_blocks, 2, n_kv, block_size, head_dim] bf16 (written in place at each
+    token's row). Returns q_out [T, n_q, head_dim] bf16."""
+    T = qkv.shape[0]
+    for name, t in (("qkv", qkv), ("kv_cache", kv_cache)) + ((("bias", bias),) if bias is not None else ()):
+        if t.dtype != torch.bfloat16:
+            raise TypeError(f"{name} must be bf16")
+    for name, t in (("positions", positions), ("block_table", block_table)):
+        if t.dtype != torch.int32:
+            raise TypeError(f"{name} must be int32")
+    if kv_cache.dim() != 5 or kv_cache.shape[1] != 2 or kv_cache.shape[2] != n_kv or kv_cache.shape[4] != head_dim:
+        raise ValueError("kv_cache must be [num_blocks, 2, n_kv, block_size, head_dim]")
+    if qkv.shape[1] != (n_q + 2 * n_kv) * head_dim or positions.shape != (T,) or block_table.shape[0] != T:
+        raise ValueError("qkv, positions and block_table shapes do not match")
+    if q_out is None:
+        q_out = torch.empty((T, n_q, head_dim), dtype=torch.bfloat16, device=qkv.device)
+    d = _lib.rope_desc(T, n_q, n_kv, head_dim, kv_cache.shape[3], block_table.shape[1], kv_cache.shape[0],
+                       rope_base, interleaved)
+    _lib.bias_rope_kv_update(d, _dev(qkv, "qkv"), _dev(bias, "bias"), _dev(positions, "positions"),
+                             _dev(block_table, "block_table"), _dev(q_out, "q_out"), _dev(kv_cache, "kv_cache"),
+                             _stream(stream))
+    return q_out

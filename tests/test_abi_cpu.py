@@ -215,3 +215,39 @@ def test_moe_workspace_and_validation():
     with pytest.raises(L.FgError) as ei:                                   # misaligned tokens
         L.moe_grouped_ffn(d, fake + 4, *([fake] * 11), 1 << 30, None)
     assert ei.value.status == L.FG_ERR_ALIGNMENT
+
+
+def test_rope_kv_validation():
+    fake = 1 << 40
+
+    def st(desc, qkv=fake, bias=fake, pos=fake, table=fake, q=fake, cache=fake):
+        try:
+            L.bias_rope_kv_update(desc, qkv, bias, pos, table, q, cache)
+            return L.FG_OK
+        except L.FgError as e:
+            return e.status
+
+    D = lambda **kw: L.rope_desc(**{**dict(T=4, n_q=64, n_kv=8, D=64, block_size=64, max_blocks=8,  # noqa: E731
+                                          num_blocks=16, base=150000.0), **kw})
+    assert st(D(T=0), None, None, None, None, None, None) == L.FG_OK          # nothing to do
+    assert st(None) == L.FG_ERR_INVALID_ARG
+    assert st(D(T=-1)) == L.FG_ERR_INVALID_ARG
+    assert st(D(n_q=0)) == L.FG_ERR_INVALID_ARG
+    assert st(D(n_kv=0)) == L.FG_ERR_INVALID_ARG
+    assert st(D(D=8)) == L.FG_ERR_INVALID_ARG
+    assert st(D(D=72)) == L.FG_ERR_ALIGNMENT                                  # not a multiple of 16
+    assert st(D(D=272)) == L.FG_ERR_UNSUPPORTED
+    assert st(D(block_size=0)) == L.FG_ERR_INVALID_ARG
+    assert st(D(max_blocks=0)) == L.FG_ERR_INVALID_ARG
+    assert st(D(num_blocks=0)) == L.FG_ERR_INVALID_ARG
+    assert st(D(base=0.0)) == L.FG_ERR_INVALID_ARG
+    assert st(D(base=float("inf"))) == L.FG_ERR_INVALID_ARG
+    d = D()
+    d.interleaved = 2
+    assert st(d) == L.FG_ERR_INVALID_ARG
+    assert st(D(), qkv=None) == L.FG_ERR_INVALID_ARG
+    assert st(D(), cache=None) == L.FG_ERR_INVALID_ARG
+    assert st(D(), qkv=fake + 8) == L.FG_ERR_ALIGNMENT
+    assert st(D(), bias=fake + 2) == L.FG_ERR_ALIGNMENT
+    assert st(D(), pos=fake + 2) == L.FG_ERR_ALIGNMENT
+    assert "bias_rope_kv_update" in L.last_error()
