@@ -49,6 +49,7 @@ struct DenseArgs {
   int M, N;
   int64_t K;
   int tiles_m, tiles_n;
+  int group_m;            // m-tiles per raster group (see tile_coords)
   int ks;                 // K slices (1 = no split)
   int64_t kslice;         // bytes of each row per slice but the last (multiple of 128)
   unsigned long long* counters;  // [tiles] (epoch << 32 | arrivals) words (split-K only)
@@ -64,6 +65,20 @@ struct DenseArgs {
 // tile share one L2 and so do the tiles that reuse the same W columns.
 __device__ __forceinline__ int xcd_order(int b, int G) {
   return (G & 7) == 0 ? (b & 7) * (G >> 3) + (b >> 3) : b;
+}
+
+// Output tile of tile index `tile`: the tiles are walked in groups of GM
+// tile rows, m fastest inside a group, so any run of consecutive indices —
+// the tiles one XCD holds at a time — covers a block about GM rows tall and
+// run/GM columns wide instead of a strip one or two columns wide. The L2 of
+// that XCD then fetches GM row tiles of A and run/GM column tiles of W per
+// K stage. The last group may be shorter.
+__device__ __forceinline__ void tile_coords(int tile, int tiles_m, int tiles_n, int GM, int& tm, int& tn) {
+  const int per_group = GM * tiles_n;
+  const int g = tile / per_group, local = tile - g * per_group;
+  const int rows = tiles_m - g * GM < GM ? tiles_m - g * GM : GM;
+  tm = g * GM + local % rows;
+  tn = local / rows;
 }
 
 // Split-K exchange. Every slice stores its partial tile with device-coherent
@@ -146,7 +161,8 @@ __global__ __launch_bounds__(TL::THREADS) void fgemm_kernel(DenseArgs a, EpiArgs
   __shared__ __attribute__((aligned(16))) char lds[DenseLds<TL>::BYTES];
   const int t = xcd_order(blockIdx.x, a.tiles_m * a.tiles_n * a.ks);
   const int ks = t % a.ks, tile = t / a.ks;
-  const int tm = tile % a.tiles_m, tn = tile / a.tiles_m;
+  int tm, tn;
+  tile_coords(tile, a.tiles_m, a.tiles_n, a.group_m, tm, tn);
   const int m0 = tm * TL::BM, n0 = tn * TL::BN;
   const int64_t rowbytes = a.K * TL::ESIZE;
   const int64_t kbeg = ks * a.kslice;
@@ -481,6 +497,7 @@ extern "C" fg_status fgemm_run(const fg_plan* plan, const void* A, const void* W
   a.N = (int)p.N;
   a.K = p.K;
   a.tiles_m = (int)p.tiles_m;
+  a.group_m = (int)(p.tiles_m < 4 ? p.tiles_m : 4);
   a.tiles_n = (int)p.tiles_n;
   a.ks = p.ks;
   a.kslice = p.kslice;
