@@ -101,6 +101,17 @@ def time_steps(fn, steps, warmup, torch):
     return start.elapsed_time(stop) / steps      # ms per step
 
 
+def repeat_stats(fn, steps, torch, count=7):
+    """Seven further timings of `steps` steps each, after the reported one:
+    the median step time and the coefficient of variation across them (the
+    run-to-run spread on one box; the reported value is the first timing)."""
+    import statistics
+    ms = [time_steps(fn, steps, 0, torch) for _ in range(count)]
+    med = statistics.median(ms)
+    cv = statistics.pstdev(ms) / statistics.fmean(ms)
+    return {"count": count, "ms_per_step_median": round(med, 5), "cv": round(cv, 5)}
+
+
 FGEMM_WORKLOADS = {"gelu_clamp": "bf16_gelu_clamp", "lse": "bf16_lse", "silu_gn": "bf16_silu_gn",
                    "tiny_f32": "tiny_f32_relu_x2", "scale_lse_mish": "bf16_scale_lse_mish",
                    "gn_swish_mul_swish": "bf16_gn_swish_mul_swish", "gn_lrelu_sum": "bf16_gn_lrelu_sum",
@@ -153,6 +164,7 @@ def bench_fgemm(args, torch, np):
 
     settle(fused, args.warmup_seconds, torch)
     ms = time_steps(fused, args.steps, args.warmup, torch)
+    reps = repeat_stats(fused, args.steps, torch)
     flops = spec.flops()
     tflops = flops / (ms * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if spec.dtype == "bf16" else 157.3
@@ -171,6 +183,7 @@ def bench_fgemm(args, torch, np):
         {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
          "frac": round(achieved / peak, 4), "traffic": measured_traffic(name),
          "algorithmic_flops_per_launch": flops, "algorithmic_bytes_per_launch": spec.bytes()})
+    result["repeats"] = reps
 
     if not args.no_unfused:
         tdt = torch.float32 if spec.dtype == "f32" else torch.bfloat16
@@ -277,6 +290,7 @@ def bench_moe(args, torch, np):
 
     settle(fused, args.warmup_seconds, torch)
     ms = time_steps(fused, args.steps, args.warmup, torch)
+    reps = repeat_stats(fused, args.steps, torch)
     counts = np.diff(bufs.offsets.cpu().numpy())
     active = int(np.sum(counts > 0))
     flops = spec.flops()
@@ -299,6 +313,7 @@ def bench_moe(args, torch, np):
                      f"{spec.w_dtype} weights, clamped SwiGLU",
          "T": spec.T, "H": spec.H, "I": spec.I, "E": spec.E, "top_k": spec.k}, roof)
     result["hbm_gbs"] = round(gbs, 1)
+    result["repeats"] = reps
 
     if not args.no_unfused and spec.w_dtype == "bf16":
         # The eager PyTorch sequence: top-k and softmax, a stable argsort of the
