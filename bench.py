@@ -314,6 +314,11 @@ def bench_moe(args, torch, np):
          "T": spec.T, "H": spec.H, "I": spec.I, "E": spec.E, "top_k": spec.k}, roof)
     result["hbm_gbs"] = round(gbs, 1)
     result["repeats"] = reps
+    if not args.no_cpu_baseline:
+        torch.cuda.synchronize()
+        cpu, rep = cpu_oracle_moe(spec, act, bufs.out, nbytes, decode, np, torch)
+        result["cpu_baseline"] = cpu
+        result["parity_sample"] = {"rel_err": rep.rel_err, "tol": rep.tol, "ok": bool(rep.ok)}
 
     if not args.no_unfused and spec.w_dtype == "bf16":
         # The eager PyTorch sequence: top-k and softmax, a stable argsort of the
@@ -353,6 +358,44 @@ def bench_moe(args, torch, np):
                                          "scatter, slot sum"}
         result["speedup_vs_unfused"] = round(ms_u / ms, 3)
     return result
+
+
+def cpu_oracle_moe(spec, act, out, step_bytes, decode, np, torch):
+    """Time the fp64 oracle's MoE step on the host: the whole step at decode
+    size (T = 64), the first 64 tokens of the prefill batch otherwise. The
+    oracle decodes each expert's weights to fp64 as part of its work."""
+    from threadpoolctl import threadpool_info
+    from oracle import bf16_decode, compare, e4m3_decode, ref_moe
+    from paper_2606_02963_amd.synth import make_moe_weights
+
+    w = make_moe_weights(spec, 0)
+    if spec.w_dtype == "bf16":
+        weights = lambda e: (bf16_decode(w["w_gate_up"][e]), bf16_decode(w["w_down"][e]))  # noqa: E731
+    else:
+        weights = lambda e: (e4m3_decode(w["w_gate_up"][e]) * w["s_gate_up"][e][:, None].astype(np.float64),  # noqa: E731
+                             e4m3_decode(w["w_down"][e]) * w["s_down"][e][:, None].astype(np.float64))
+    tokens = None if decode else np.arange(min(64, spec.T))
+    f8 = spec.w_dtype == "e4m3"
+    t0 = time.perf_counter()
+    ref = ref_moe(bf16_decode(act["x"]), act["logits"].astype(np.float64), weights, spec.k,
+                  storage="e4m3" if f8 else "bf16", act_quant=f8, alpha=spec.alpha, limit=spec.limit,
+                  tokens=tokens, with_bound=True)
+    sec = time.perf_counter() - t0
+    got = bf16_decode(out.view(torch.int16).cpu().numpy().view(np.uint16))
+    if tokens is not None:
+        got = got[tokens]
+    rep = compare(got, ref["out"], "e4m3" if f8 else "bf16", slack=ref["out_bound"])
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    n = spec.T if tokens is None else tokens.size
+    if decode:
+        value, unit = step_bytes / sec / 1e9, "GB/s"
+    else:
+        value, unit = 2.0 * n * spec.k * (spec.H * 2 * spec.I + spec.I * spec.H) / sec / 1e12, "TFLOP/s"
+    return ({"value": round(value, 4), "unit": unit, "cores": int(threads), "kind": "oracle",
+             "sample": (f"the whole T={spec.T} step" if tokens is None else
+                        f"{n} of {spec.T} tokens (their {n * spec.k} slots through all experts)") +
+                       f", fp64 numpy incl. decoding the expert weights, {sec:.1f} s",
+             "seconds": round(sec, 2)}, rep)
 
 
 def bench_finalize(args, torch, np):
