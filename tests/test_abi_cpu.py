@@ -251,3 +251,34 @@ def test_rope_kv_validation():
     assert st(D(), bias=fake + 2) == L.FG_ERR_ALIGNMENT
     assert st(D(), pos=fake + 2) == L.FG_ERR_ALIGNMENT
     assert "bias_rope_kv_update" in L.last_error()
+
+
+def test_finalize_and_rmsnorm_validation_on_the_host():
+    # every case fails (or, for T = 0, returns) before any HIP call, so fake
+    # device addresses are never touched
+    fake = 1 << 40
+    L.moe_finalize(fake, fake, 0, 16, 4, None)                              # T = 0: nothing to do
+    for args, status in [((2, 12, 4), L.FG_ERR_ALIGNMENT), ((2, 16, 9), L.FG_ERR_INVALID_ARG),
+                         ((2, 16, 0), L.FG_ERR_INVALID_ARG), ((-1, 16, 4), L.FG_ERR_INVALID_ARG)]:
+        with pytest.raises(L.FgError) as ei:
+            L.moe_finalize(fake, fake, *args, None)
+        assert ei.value.status == status
+    with pytest.raises(L.FgError) as ei:
+        L.moe_finalize(fake + 2, fake, 2, 16, 4, None)
+    assert ei.value.status == L.FG_ERR_ALIGNMENT
+    with pytest.raises(L.FgError) as ei:
+        L.moe_finalize(None, fake, 2, 16, 4, None)
+    assert ei.value.status == L.FG_ERR_INVALID_ARG
+    L.add_rmsnorm(fake, fake, fake, fake, 0, 16, 1e-5, None)               # T = 0
+    for args, status in [((2, 12, 1e-5), L.FG_ERR_ALIGNMENT), ((2, 4104, 1e-5), L.FG_ERR_UNSUPPORTED),
+                         ((2, 16, -1.0), L.FG_ERR_INVALID_ARG), ((2, 16, float("nan")), L.FG_ERR_INVALID_ARG),
+                         ((-1, 16, 1e-5), L.FG_ERR_INVALID_ARG)]:
+        with pytest.raises(L.FgError) as ei:
+            L.add_rmsnorm(fake, fake, fake, fake, *args, None)
+        assert ei.value.status == status
+    with pytest.raises(L.FgError) as ei:
+        L.add_rmsnorm(fake + 2, fake, fake, fake, 2, 16, 1e-5, None)
+    assert ei.value.status == L.FG_ERR_ALIGNMENT
+    with pytest.raises(L.FgError) as ei:
+        L.add_rmsnorm(None, fake, fake, fake, 2, 16, 1e-5, None)
+    assert ei.value.status == L.FG_ERR_INVALID_ARG
