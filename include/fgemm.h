@@ -135,7 +135,8 @@ size_t fgemm_workspace_bytes(const fg_plan *plan);
  *   A      [M, K] in_dtype.      W      [N, K] in_dtype (both may be NULL when K = 0).
  *   bias   [N] fp32, required iff epi.has_bias (else ignored, may be NULL).
  *   gamma, beta  [N] fp32, required iff GroupNorm (else ignored).
- *   out    [M, N] out_dtype, or [M] fp32 for LogSumExp.
+ *   out    [M, N] out_dtype, or [M] fp32 for LogSumExp; must not overlap A,
+ *          W, bias, gamma, beta or the workspace.
  *   workspace, ws_bytes  device scratch of at least fgemm_workspace_bytes;
  *          may be NULL when that is 0. Contents on entry are ignored: the
  *          split-K arrival counters carry a per-run epoch, so values left by
@@ -187,7 +188,8 @@ size_t moe_workspace_bytes(const moe_desc *d);
  *   w_down         [E, H, I] bf16, or e4m3 codes.
  *   s_gateup       [E, 2I] fp32 per-row weight scales (e4m3 only, else NULL).
  *   s_down         [E, H] fp32 per-row weight scales (e4m3 only, else NULL).
- *   out            [T, H] bf16: out[t] = Σ_j w[t,j]·FFN_{idx[t,j]}(tokens[t]).
+ *   out            [T, H] bf16: out[t] = Σ_j w[t,j]·FFN_{idx[t,j]}(tokens[t]);
+ *                  no output or workspace may overlap an input or each other.
  *   topk_idx       [T, top_k] int32 out: selected experts, logits descending,
  *                  ties to the lower expert index (a NaN logit ranks as −∞).
  *   topk_w         [T, top_k] fp32 out: softmax over the selected logits.
