@@ -12,7 +12,7 @@ roofline fraction against the dense bf16 MFMA peak, the unfused sequence
 it, and the fp64 CPU oracle timed on a bounded sample of rows.
 
 Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
-                       [--workload gelu_clamp|lse|silu_gn|tiny_f32|scale_lse_mish|gn_swish_mul_swish|
+                       [--workload gelu_clamp|gelu_clamp_e4m3|lse|silu_gn|tiny_f32|scale_lse_mish|gn_swish_mul_swish|
                                    gn_lrelu_sum|swish_sum_gn|moe_{prefill,decode}_{bf16,e4m3}|
                                    moe_finalize|add_rmsnorm|rope_kv]
 """
@@ -28,6 +28,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published
+PEAK_FP8_TFLOPS = 5000.0       # MI355X dense fp8 MFMA, published
 PEAK_HBM_GBS = 8000.0
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = ["fg_tile.hpp", "fg_epilogue.hpp", "fgemm.hip"]
@@ -48,7 +49,7 @@ def parse():
                     help="after the measurement, run a plain device-to-device copy of this many MiB "
                          "(3 times); its HBM counters calibrate rocprofv3 FETCH_SIZE/WRITE_SIZE")
     ap.add_argument("--workload", default="gelu_clamp",
-                    choices=["gelu_clamp", "lse", "silu_gn", "tiny_f32", "scale_lse_mish",
+                    choices=["gelu_clamp", "gelu_clamp_e4m3", "lse", "silu_gn", "tiny_f32", "scale_lse_mish",
                              "gn_swish_mul_swish", "gn_lrelu_sum", "swish_sum_gn", "moe_prefill_bf16",
                              "moe_prefill_e4m3", "moe_decode_bf16", "moe_decode_e4m3", "moe_finalize", "add_rmsnorm",
                              "rope_kv"],
@@ -115,14 +116,15 @@ def repeat_stats(fn, steps, torch, count=7):
 FGEMM_WORKLOADS = {"gelu_clamp": "bf16_gelu_clamp", "lse": "bf16_lse", "silu_gn": "bf16_silu_gn",
                    "tiny_f32": "tiny_f32_relu_x2", "scale_lse_mish": "bf16_scale_lse_mish",
                    "gn_swish_mul_swish": "bf16_gn_swish_mul_swish", "gn_lrelu_sum": "bf16_gn_lrelu_sum",
-                   "swish_sum_gn": "bf16_swish_sum_gn"}
+                   "swish_sum_gn": "bf16_swish_sum_gn", "gelu_clamp_e4m3": "e4m3_gelu_clamp"}
 MOE_WORKLOADS = {"moe_prefill_bf16", "moe_prefill_e4m3", "moe_decode_bf16", "moe_decode_e4m3"}
 TAIL_TEXT = {"bf16_gelu_clamp": "(x0.5, GELU_tanh, clamp[-1,1])", "bf16_lse": "(-0.25, row logsumexp)",
              "bf16_silu_gn": "(SiLU, GroupNorm 32x128)", "tiny_f32_relu_x2": "(ReLU, x2)",
              "bf16_scale_lse_mish": "(x2, row logsumexp, Mish)",
              "bf16_gn_swish_mul_swish": "(GroupNorm 32x128, SiLU, x1.5, SiLU)",
              "bf16_gn_lrelu_sum": "(GroupNorm 32x128, LeakyReLU 0.01, x+x)",
-             "bf16_swish_sum_gn": "(SiLU, +0.25, GroupNorm 32x128)"}
+             "bf16_swish_sum_gn": "(SiLU, +0.25, GroupNorm 32x128)",
+             "e4m3_gelu_clamp": "(per-row scales, x0.5, GELU_tanh, clamp[-1,1])"}
 
 
 def base_result(args, metric_value, ms, dtype, data, config, roofline):
@@ -143,8 +145,12 @@ def bench_fgemm(args, torch, np):
     spec = FGEMM_SPECS[FGEMM_WORKLOADS[args.workload]]
     inp = make_fgemm_inputs(spec, seed=0)
     dev = torch.device("cuda", 0)
+    sx = sw = None
     if spec.dtype == "f32":
         x, W = torch.from_numpy(inp["x"]).to(dev), torch.from_numpy(inp["W"]).to(dev)
+    elif spec.dtype == "e4m3":
+        x, W = torch.from_numpy(inp["x"]).to(dev), torch.from_numpy(inp["W"]).to(dev)
+        sx, sw = torch.from_numpy(inp["x_scale"]).to(dev), torch.from_numpy(inp["w_scale"]).to(dev)
     else:
         x = torch.from_numpy(inp["x"].view(np.int16)).view(torch.bfloat16).to(dev)
         W = torch.from_numpy(inp["W"].view(np.int16)).view(torch.bfloat16).to(dev)
@@ -160,14 +166,15 @@ def bench_fgemm(args, torch, np):
 
     def fused():
         api.linear_epilogue(x, W, b, spec.ops, spec.reduction, spec.gn_groups, spec.gn_eps, g, be,
-                            out_dtype=spec.out, out=out, workspace=ws, post_ops=spec.post_ops)
+                            out_dtype=spec.out, out=out, workspace=ws, post_ops=spec.post_ops,
+                            x_scale=sx, w_scale=sw)
 
     settle(fused, args.warmup_seconds, torch)
     ms = time_steps(fused, args.steps, args.warmup, torch)
     reps = repeat_stats(fused, args.steps, torch)
     flops = spec.flops()
     tflops = flops / (ms * 1e-3) / 1e12
-    peak = PEAK_BF16_TFLOPS if spec.dtype == "bf16" else 157.3
+    peak = {"bf16": PEAK_BF16_TFLOPS, "e4m3": PEAK_FP8_TFLOPS, "f32": 157.3}[spec.dtype]
     # the GEMM launch dominates; with a row LogSumExp the step also holds the
     # small combine launch, so the step time bounds the GEMM launch from above
     achieved = tflops
@@ -209,8 +216,20 @@ def bench_fgemm(args, torch, np):
                     z = F.leaky_relu(z, op[1])
             return z
 
+        if spec.dtype == "e4m3":
+            # vendor fp8 GEMM with row-wise scales (hipBLASLt through
+            # torch._scaled_mm), bf16 result
+            x8, W8 = x.view(torch.float8_e4m3fn), W.view(torch.float8_e4m3fn)
+            sa, sb = sx.view(-1, 1), sw.view(1, -1)
+
+            def vendor_mm():
+                return torch._scaled_mm(x8, W8.t(), scale_a=sa, scale_b=sb, out_dtype=torch.bfloat16)
+        else:
+            def vendor_mm():
+                return torch.mm(x, W.t())
+
         def unfused():
-            z = torch.mm(x, W.t())
+            z = vendor_mm()
             z = eager_ops(z + bb, spec.ops)
             if spec.reduction == "lse":
                 z = torch.logsumexp(z.float(), dim=1)
@@ -218,15 +237,18 @@ def bench_fgemm(args, torch, np):
                 z = F.group_norm(z, spec.gn_groups, g.to(tdt), be.to(tdt), spec.gn_eps)
             return eager_ops(z, spec.post_ops)
 
-        def gemm_only():
-            return torch.mm(x, W.t())
-
-        ms_u = time_steps(unfused, args.steps, args.warmup, torch)
-        ms_g = time_steps(gemm_only, args.steps, args.warmup, torch)
-        result["unfused"] = {"ms": round(ms_u, 5), "tflops": round(flops / (ms_u * 1e-3) / 1e12, 2),
-                             "sequence": "torch.mm (vendor BLAS) then one eager kernel per tail op"}
-        result["gemm_only"] = {"ms": round(ms_g, 5), "tflops": round(flops / (ms_g * 1e-3) / 1e12, 2)}
-        result["speedup_vs_unfused"] = round(ms_u / ms, 3)
+        try:
+            ms_u = time_steps(unfused, args.steps, args.warmup, torch)
+            ms_g = time_steps(vendor_mm, args.steps, args.warmup, torch)
+        except RuntimeError as e:         # a torch build without row-wise fp8 scaling
+            result["unfused"] = {"ms": None, "error": str(e).splitlines()[0][:200]}
+        else:
+            result["unfused"] = {"ms": round(ms_u, 5), "tflops": round(flops / (ms_u * 1e-3) / 1e12, 2),
+                                 "sequence": ("torch._scaled_mm (vendor fp8 GEMM, row-wise scales)"
+                                              if spec.dtype == "e4m3" else "torch.mm (vendor BLAS)")
+                                 + " then one eager kernel per tail op"}
+            result["gemm_only"] = {"ms": round(ms_g, 5), "tflops": round(flops / (ms_g * 1e-3) / 1e12, 2)}
+            result["speedup_vs_unfused"] = round(ms_u / ms, 3)
 
     if not args.no_cpu_baseline:
         torch.cuda.synchronize()
@@ -239,10 +261,14 @@ def bench_fgemm(args, torch, np):
 def cpu_oracle_fgemm(spec, inp, budget_s, out, np):
     """Time the fp64 oracle on a growing sample of rows until ~budget_s."""
     from threadpoolctl import threadpool_info
-    from oracle import bf16_decode, compare, ref_fgemm
+    from oracle import bf16_decode, compare, e4m3_decode, ref_fgemm
 
-    dec = (lambda a: a.astype(np.float64)) if spec.dtype == "f32" else bf16_decode
-    x64, W64 = dec(inp["x"]), dec(inp["W"])
+    if spec.dtype == "e4m3":
+        x64 = e4m3_decode(inp["x"]) * inp["x_scale"].astype(np.float64)[:, None]
+        W64 = e4m3_decode(inp["W"]) * inp["w_scale"].astype(np.float64)[:, None]
+    else:
+        dec = (lambda a: a.astype(np.float64)) if spec.dtype == "f32" else bf16_decode
+        x64, W64 = dec(inp["x"]), dec(inp["W"])
     b = inp["b"].astype(np.float64)
     got = out.float().cpu().numpy().astype(np.float64)
     rows, t_total, flops_total, n_rows, first = 8, 0.0, 0.0, 0, None
@@ -259,7 +285,7 @@ def cpu_oracle_fgemm(spec, inp, budget_s, out, np):
         n_rows += r
         rows *= 2
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    rep = compare(got[first[0]], first[1], "f32" if spec.dtype == "f32" else "bf16")
+    rep = compare(got[first[0]], first[1], {"f32": "f32", "bf16": "bf16", "e4m3": "e4m3"}[spec.dtype])
     return ({"value": flops_total / t_total / 1e12, "unit": "TFLOP/s", "cores": int(threads),
              "kind": "oracle",
              "sample": f"{n_rows} of {spec.M} output rows (all {spec.N} columns, K={spec.K}), "

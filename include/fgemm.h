@@ -112,9 +112,12 @@ typedef struct fg_plan fg_plan; /* opaque, host memory, immutable once built */
  *   M, N, K  x is [M, K], W is [N, K], output [M, N] (or [M] for LSE).
  *            M = 0 is a valid empty problem (fgemm_run enqueues nothing);
  *            K = 0 gives z = b. Each must be < 2^31.
- *   in_dtype FG_F32 or FG_BF16 for both x and W. K must be a multiple of 4
- *            (f32) or 8 (bf16) so that rows stay 16-byte aligned
- *            (FG_ERR_ALIGNMENT otherwise).
+ *   in_dtype FG_F32, FG_BF16 or FG_E4M3 for both x and W. K must be a
+ *            multiple of 4 (f32), 8 (bf16) or 16 (e4m3) so that rows stay
+ *            16-byte aligned (FG_ERR_ALIGNMENT otherwise). FG_E4M3 is the W8A8
+ *            form: OCP e4m3fn codes with one fp32 scale per row of x and per
+ *            row of W, run with fgemm_run_scaled; the fp8 MFMA accumulates in
+ *            fp32 and z = (Σ_k qx·qw)·sx[m]·sw[n] + b before the tail.
  *   out_dtype FG_F32 or FG_BF16; LogSumExp requires FG_F32. N must be a
  *            multiple of 4 (f32 out) or 8 (bf16 out) (FG_ERR_ALIGNMENT).
  *   epi      the tail (copied into the plan; the caller keeps ownership).
@@ -148,6 +151,20 @@ size_t fgemm_workspace_bytes(const fg_plan *plan);
 fg_status fgemm_run(const fg_plan *plan, const void *A, const void *W,
                     const float *bias, const float *gamma, const float *beta,
                     void *out, void *workspace, size_t ws_bytes, void *stream);
+
+/*
+ * fgemm_run_scaled — fgemm_run with per-row scales, required for FG_E4M3
+ * plans (and ignored, may be NULL, for f32 / bf16 plans):
+ *   a_scale  [M] fp32: x[m, k] = codes_x[m, k]·a_scale[m];
+ *   w_scale  [N] fp32: W[n, k] = codes_w[n, k]·w_scale[n];
+ * every other argument as for fgemm_run (A and W are the uint8 codes).
+ * FG_ERR_INVALID_ARG for an e4m3 plan without both scales; fgemm_run on an
+ * e4m3 plan returns the same status.
+ */
+fg_status fgemm_run_scaled(const fg_plan *plan, const void *A, const void *W,
+                           const float *a_scale, const float *w_scale,
+                           const float *bias, const float *gamma, const float *beta,
+                           void *out, void *workspace, size_t ws_bytes, void *stream);
 
 void fgemm_destroy(fg_plan *plan);
 

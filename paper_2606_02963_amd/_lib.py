@@ -70,6 +70,8 @@ def lib():
         L.fgemm_workspace_bytes.restype = sz
         L.fgemm_run.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.fgemm_run.restype = i32
+        L.fgemm_run_scaled.argtypes = [vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+        L.fgemm_run_scaled.restype = i32
         L.fgemm_destroy.argtypes = [vp]
         L.fgemm_destroy.restype = None
         L.fgemm_plan_info.argtypes = [vp, C.POINTER(i32), C.POINTER(i32), C.POINTER(i64), C.POINTER(i32),
@@ -182,6 +184,13 @@ def fgemm_workspace_bytes(plan):
 def fgemm_run(plan, A, W, bias, gamma, beta, out, workspace, ws_bytes, stream=None):
     st = lib().fgemm_run(plan.handle, A, W, bias, gamma, beta, out, workspace, ws_bytes, stream)
     _check(st, "fgemm_run")
+
+
+def fgemm_run_scaled(plan, A, W, a_scale, w_scale, bias, gamma, beta, out, workspace, ws_bytes, stream=None):
+    """fgemm_run with per-row scales of x and W (required for e4m3 plans)."""
+    st = lib().fgemm_run_scaled(plan.handle, A, W, a_scale, w_scale, bias, gamma, beta, out, workspace,
+                                ws_bytes, stream)
+    _check(st, "fgemm_run_scaled")
 
 
 def moe_desc(T, H, I, E, top_k, w_dtype="bf16", alpha=1.702, limit=7.0, interleaved=False):

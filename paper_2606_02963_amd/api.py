@@ -53,19 +53,22 @@ def get_plan(M, N, K, in_dtype, out_dtype, has_bias, ops=(), reduction=None, gn_
 
 def linear_epilogue(x, W, bias=None, ops=(), reduction=None, gn_groups=0, gn_eps=1e-5,
                     gamma=None, beta=None, out_dtype=None, out=None, workspace=None, stream=None,
-                    post_ops=()):
+                    post_ops=(), x_scale=None, w_scale=None):
     """y = tail(x·Wᵀ + b) in one fused launch (two for a row LogSumExp).
 
-    x [M, K] and W [N, K] (f32 or bf16, same dtype), bias/gamma/beta fp32 [N].
-    ops: ((kind, a, b), ...) with kinds scale, add, relu, gelu_tanh, silu,
-    clamp, mish, leaky_relu. reduction: None, "lse" (returns fp32 [M]) or
-    "groupnorm". post_ops: ops of the same kinds applied to the reduction's
-    result."""
+    x [M, K] and W [N, K] (f32 or bf16, same dtype; or e4m3 codes as uint8
+    with per-row fp32 scales x_scale [M] and w_scale [N]), bias/gamma/beta
+    fp32 [N]. ops: ((kind, a, b), ...) with kinds scale, add, relu,
+    gelu_tanh, silu, clamp, mish, leaky_relu. reduction: None, "lse"
+    (returns fp32 [M]) or "groupnorm". post_ops: ops of the same kinds
+    applied to the reduction's result."""
     M, K = x.shape
     N, K2 = W.shape
     if K2 != K or x.dtype != W.dtype:
         raise ValueError("x must be [M,K] and W [N,K] of one dtype")
     in_dt = _dt_name(x)
+    if in_dt == "e4m3" and (x_scale is None or w_scale is None):
+        raise ValueError("e4m3 inputs need x_scale [M] and w_scale [N]")
     if out_dtype is None:
         out_dtype = "f32" if (in_dt == "f32" or reduction == "lse") else "bf16"
     plan = get_plan(M, N, K, in_dt, out_dtype, bias is not None, ops, reduction, gn_groups, gn_eps,
@@ -76,9 +79,9 @@ def linear_epilogue(x, W, bias=None, ops=(), reduction=None, gn_groups=0, gn_eps
     ws_bytes = plan.workspace_bytes()
     if ws_bytes and workspace is None:
         workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=x.device)
-    _lib.fgemm_run(plan, _dev(x, "x"), _dev(W, "W"), _dev(bias, "bias"), _dev(gamma, "gamma"),
-                   _dev(beta, "beta"), _dev(out, "out"), _dev(workspace, "workspace"),
-                   ws_bytes, _stream(stream))
+    _lib.fgemm_run_scaled(plan, _dev(x, "x"), _dev(W, "W"), _dev(x_scale, "x_scale"), _dev(w_scale, "w_scale"),
+                          _dev(bias, "bias"), _dev(gamma, "gamma"), _dev(beta, "beta"), _dev(out, "out"),
+                          _dev(workspace, "workspace"), ws_bytes, _stream(stream))
     return out
 
 

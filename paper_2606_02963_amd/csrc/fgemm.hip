@@ -44,6 +44,8 @@ struct DenseArgs {
   const float* bias;
   const float* gamma;
   const float* beta;
+  const float* a_scale;   // e4m3: per-row scale of x [M]
+  const float* w_scale;   // e4m3: per-row scale of W [N]
   void* out;
   float2* ws;
   int M, N;
@@ -173,10 +175,36 @@ __global__ __launch_bounds__(TL::THREADS) void fgemm_kernel(DenseArgs a, EpiArgs
   ra.init(a.A + (int64_t)m0 * rowbytes + kbeg, a.M - m0, TL::BM, rowbytes);
   rb.init(a.W + (int64_t)n0 * rowbytes + kbeg, a.N - n0, TL::BN, rowbytes);
 
+  // e4m3 (W8A8): the per-row scales of x and W, loaded before the K loop so
+  // that their latency hides behind it
+  float rsc[TL::IN == In::E4M3 ? TL::FM : 1][4], csc[TL::IN == In::E4M3 ? TL::FN : 1];
+  if constexpr (TL::IN == In::E4M3) {
+#pragma unroll
+    for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = m0 + acc_row<TL>(fm, i);
+        rsc[fm][i] = m < a.M ? a.a_scale[m] : 0.0f;
+      }
+#pragma unroll
+    for (int fn = 0; fn < TL::FN; ++fn) {
+      const int n = n0 + acc_col<TL>(fn);
+      csc[fn] = n < a.N ? a.w_scale[n] : 0.0f;
+    }
+  }
+
   f32x4 acc[TL::FM][TL::FN];
   gemm_mainloop<TL>(ra, rb, kbytes, lds, acc);
   if (a.ks > 1 && !split_k_gather<TL>(a, tile, ks, acc, reinterpret_cast<unsigned*>(lds))) return;
 
+  if constexpr (TL::IN == In::E4M3) {
+#pragma unroll
+    for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+      for (int fn = 0; fn < TL::FN; ++fn)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[fm][fn][i] *= rsc[fm][i] * csc[fn];
+  }
   if (a.bias != nullptr) add_bias<TL>(a.bias, n0, a.N, acc);
   apply_ops<TL>(ep, acc);
 
@@ -251,8 +279,17 @@ typedef Tile<In::F32, 64, 128> TileF32;
 typedef Tile<In::BF16, 256, 256, 2, 4> TileHuge;
 typedef Tile<In::BF16, 256, 128, 4, 2> TileBig;
 typedef Tile<In::BF16, 128, 128> TileMid;
+typedef Tile<In::E4M3, 256, 128, 4, 2> TileF8Big;
+typedef Tile<In::E4M3, 128, 128> TileF8Mid;
 
-enum Cfg : int { CFG_F32 = 0, CFG_BF16_256x128 = 1, CFG_BF16_128x128 = 2, CFG_BF16_256x256 = 3 };
+enum Cfg : int {
+  CFG_F32 = 0,
+  CFG_BF16_256x128 = 1,
+  CFG_BF16_128x128 = 2,
+  CFG_BF16_256x256 = 3,
+  CFG_E4M3_256x128 = 4,
+  CFG_E4M3_128x128 = 5
+};
 
 // Relative MFMA efficiency of the bf16 tiles, measured on 1024..4096-row
 // problems: the larger tile moves fewer bytes from L2 into LDS per FLOP.
@@ -264,6 +301,11 @@ static const TileModel kBf16Tiles[] = {
     {CFG_BF16_256x256, 256, 256, 1.00},
     {CFG_BF16_256x128, 256, 128, 0.88},
     {CFG_BF16_128x128, 128, 128, 0.72},
+};
+// e4m3 tiles (W8A8): relative efficiencies measured on the 1024-row shape.
+static const TileModel kE4m3Tiles[] = {
+    {CFG_E4M3_256x128, 256, 128, 0.88},
+    {CFG_E4M3_128x128, 128, 128, 0.72},
 };
 
 typedef void (*KernelFn)(DenseArgs, EpiArgs, EpiArgs);
@@ -330,9 +372,8 @@ extern "C" fg_status fgemm_plan(fg_plan** plan, int64_t M, int64_t N, int64_t K,
   if (M < 0 || N <= 0 || K < 0 || M > LIM || N > LIM || K > LIM)
     return fail(FG_ERR_INVALID_ARG, "fgemm_plan: bad shape M=%lld N=%lld K=%lld", (long long)M,
                 (long long)N, (long long)K);
-  if (in_dtype != FG_F32 && in_dtype != FG_BF16)
-    return fail(in_dtype == FG_E4M3 ? FG_ERR_UNSUPPORTED : FG_ERR_INVALID_ARG,
-                "fgemm_plan: input dtype %d not supported (f32 or bf16)", in_dtype);
+  if (in_dtype != FG_F32 && in_dtype != FG_BF16 && in_dtype != FG_E4M3)
+    return fail(FG_ERR_INVALID_ARG, "fgemm_plan: input dtype %d not supported (f32, bf16 or e4m3)", in_dtype);
   if (out_dtype != FG_F32 && out_dtype != FG_BF16)
     return fail(FG_ERR_INVALID_ARG, "fgemm_plan: output dtype %d not supported (f32 or bf16)", out_dtype);
   if (epi->n_ops < 0 || epi->n_ops > FG_MAX_OPS)
@@ -362,11 +403,12 @@ extern "C" fg_status fgemm_plan(fg_plan** plan, int64_t M, int64_t N, int64_t K,
     return fail(FG_ERR_INVALID_ARG, "fgemm_plan: post ops need a reduction (append them to ops instead)");
   if (red == FG_RED_LOGSUMEXP_ROW && out_dtype != FG_F32)
     return fail(FG_ERR_INVALID_ARG, "fgemm_plan: LogSumExp output must be f32");
-  const int epc = in_dtype == FG_F32 ? 4 : 8;
+  const int64_t esize = in_dtype == FG_F32 ? 4 : in_dtype == FG_BF16 ? 2 : 1;
+  const int epc = (int)(16 / esize);
   if (K % epc != 0)
     return fail(FG_ERR_ALIGNMENT, "fgemm_plan: K=%lld must be a multiple of %d", (long long)K, epc);
   // tile operands are addressed with 32-bit offsets from the tile's first row
-  if (K * (in_dtype == FG_F32 ? 4 : 2) > (int64_t)(1 << 22))
+  if (K * esize > (int64_t)(1 << 22))
     return fail(FG_ERR_UNSUPPORTED, "fgemm_plan: K=%lld exceeds the 4 MiB row limit", (long long)K);
   if (red != FG_RED_LOGSUMEXP_ROW) {
     const int opc = out_dtype == FG_F32 ? 4 : 8;
@@ -398,6 +440,20 @@ extern "C" fg_status fgemm_plan(fg_plan** plan, int64_t M, int64_t N, int64_t K,
     p->cfg = CFG_F32;
     p->BM = TileF32::BM;
     p->BN = TileF32::BN;
+  } else if (in_dtype == FG_E4M3) {
+    // W8A8: the tile that minimises workgroups per compute unit × tile work
+    // / tile efficiency; no K split
+    double best = 0.0;
+    for (const TileModel& tmod : kE4m3Tiles) {
+      const int64_t tiles = ((M + tmod.BM - 1) / tmod.BM) * ((N + tmod.BN - 1) / tmod.BN);
+      const double cost = (double)((tiles + 255) / 256) * tmod.BM * tmod.BN / tmod.eff;
+      if (best == 0.0 || cost < best) {
+        best = cost;
+        p->cfg = tmod.cfg;
+        p->BM = tmod.BM;
+        p->BN = tmod.BN;
+      }
+    }
   } else {
     // Estimated time of each (tile, K slices) choice: the workgroups one of
     // the 256 compute units runs × work per workgroup / tile efficiency, with
@@ -431,7 +487,6 @@ extern "C" fg_status fgemm_plan(fg_plan** plan, int64_t M, int64_t N, int64_t K,
     delete p;
     return fail(FG_ERR_INVALID_ARG, "fgemm_plan: too many tiles");
   }
-  const int64_t esize = in_dtype == FG_F32 ? 4 : 2;
   const int64_t stages = K * esize / 128;
   p->kslice = p->ks > 1 ? (stages / p->ks) * 128 : 0;
   p->lse_bytes = red == FG_RED_LOGSUMEXP_ROW ? (size_t)M * (size_t)p->tiles_n * sizeof(float2) : 0;
@@ -464,13 +519,14 @@ extern "C" fg_status fgemm_plan_info(const fg_plan* plan, int32_t* tile_m, int32
   return FG_OK;
 }
 
-extern "C" fg_status fgemm_run(const fg_plan* plan, const void* A, const void* W, const float* bias,
-                               const float* gamma, const float* beta, void* out, void* workspace,
-                               size_t ws_bytes, void* stream) {
-  clear_error();
+static fg_status run_plan(const fg_plan* plan, const void* A, const void* W, const float* a_scale,
+                          const float* w_scale, const float* bias, const float* gamma, const float* beta, void* out,
+                          void* workspace, size_t ws_bytes, void* stream) {
   if (plan == nullptr) return fail(FG_ERR_INVALID_ARG, "fgemm_run: plan is NULL");
   const fg_plan& p = *plan;
   if (p.M == 0) return FG_OK;
+  if (p.in_dt == FG_E4M3 && (a_scale == nullptr || w_scale == nullptr))
+    return fail(FG_ERR_INVALID_ARG, "fgemm_run: an e4m3 plan needs per-row scales (fgemm_run_scaled)");
   if (out == nullptr || (p.K > 0 && (A == nullptr || W == nullptr)))
     return fail(FG_ERR_INVALID_ARG, "fgemm_run: A, W (when K > 0) and out must be non-NULL");
   if (p.epi.has_bias && bias == nullptr) return fail(FG_ERR_INVALID_ARG, "fgemm_run: bias is NULL");
@@ -491,6 +547,8 @@ extern "C" fg_status fgemm_run(const fg_plan* plan, const void* A, const void* W
   a.bias = p.epi.has_bias ? bias : nullptr;
   a.gamma = gamma;
   a.beta = beta;
+  a.a_scale = a_scale;
+  a.w_scale = w_scale;
   a.out = out;
   a.ws = static_cast<float2*>(workspace);
   a.M = (int)p.M;
@@ -528,6 +586,8 @@ extern "C" fg_status fgemm_run(const fg_plan* plan, const void* A, const void* W
     case CFG_BF16_256x256: kc = pick_kernel<TileHuge>(red, out_k); break;
     case CFG_BF16_256x128: kc = pick_kernel<TileBig>(red, out_k); break;
     case CFG_BF16_128x128: kc = pick_kernel<TileMid>(red, out_k); break;
+    case CFG_E4M3_256x128: kc = pick_kernel<TileF8Big>(red, out_k); break;
+    case CFG_E4M3_128x128: kc = pick_kernel<TileF8Mid>(red, out_k); break;
   }
   if (kc.fn == nullptr) return fail(FG_ERR_UNSUPPORTED, "fgemm_run: no kernel for this plan");
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -539,4 +599,19 @@ extern "C" fg_status fgemm_run(const fg_plan* plan, const void* A, const void* W
                        (int)p.M, (int)p.tiles_n, post);
   }
   return check_launch("fgemm_run");
+}
+
+extern "C" fg_status fgemm_run(const fg_plan* plan, const void* A, const void* W, const float* bias,
+                               const float* gamma, const float* beta, void* out, void* workspace,
+                               size_t ws_bytes, void* stream) {
+  clear_error();
+  return run_plan(plan, A, W, nullptr, nullptr, bias, gamma, beta, out, workspace, ws_bytes, stream);
+}
+
+extern "C" fg_status fgemm_run_scaled(const fg_plan* plan, const void* A, const void* W, const float* a_scale,
+                                      const float* w_scale, const float* bias, const float* gamma,
+                                      const float* beta, void* out, void* workspace, size_t ws_bytes,
+                                      void* stream) {
+  clear_error();
+  return run_plan(plan, A, W, a_scale, w_scale, bias, gamma, beta, out, workspace, ws_bytes, stream);
 }

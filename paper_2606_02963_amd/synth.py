@@ -67,7 +67,7 @@ class FgemmSpec:
     M: int
     N: int
     K: int
-    dtype: str                    # "f32" or "bf16" (x, W); out dtype follows
+    dtype: str                    # "f32", "bf16" or "e4m3" (x, W); out dtype follows
     w_bound: float                # W, b ~ U(-w_bound, w_bound)
     ops: tuple                    # ((kind, a, b), ...) applied after +b
     reduction: str = None         # None | "lse" | "groupnorm"
@@ -87,8 +87,10 @@ class FgemmSpec:
 
     def bytes(self):
         """Algorithmic bytes: each input read once, the output written once."""
-        e = 4 if self.dtype == "f32" else 2
+        e = {"f32": 4, "bf16": 2, "e4m3": 1}[self.dtype]
         b = (self.M * self.K + self.N * self.K) * e + self.N * 4
+        if self.dtype == "e4m3":
+            b += (self.M + self.N) * 4            # per-row scales
         if self.reduction == "groupnorm":
             b += 2 * self.N * 4
         o = 4 if self.out == "f32" else 2
@@ -121,6 +123,11 @@ FGEMM_SPECS = {
     # GroupNorm(32 × 128, eps 1e-5)(SiLU(x·Wᵀ + b)); γ ~ U(0.5,1.5), β ~ N(0,0.1)
     "bf16_silu_gn": FgemmSpec("bf16_silu_gn", 2048, 4096, 4096, "bf16", 1 / 64,
                               (("silu",),), "groupnorm", 32, 1e-5),
+    # the GELU/clamp workload in the W8A8 form: x and W stored as e4m3 codes
+    # with one fp32 scale per row (the format of the MoE fp8 variant)
+    "e4m3_gelu_clamp": FgemmSpec("e4m3_gelu_clamp", 1024, 8192, 8192, "e4m3",
+                                 1 / math.sqrt(8192),
+                                 (("scale", 0.5), ("gelu_tanh",), ("clamp", -1.0, 1.0)), out_dtype="bf16"),
     # The four tail chains of paper Table III. Their problem shapes are not
     # in the paper; they take the shapes of the LSE and GroupNorm workloads
     # above. "Mul" is read as a scalar multiply, "Sum" as adding a constant
@@ -143,7 +150,9 @@ def make_fgemm_inputs(spec, seed=0):
     """Draw x, W, b (and γ, β for GroupNorm) for ``spec``.
 
     Returns a dict of numpy arrays in storage form: x [M,K] and W [N,K] as
-    fp32 (dtype f32) or uint16 bf16 bits (dtype bf16); b, gamma, beta fp32."""
+    fp32 (dtype f32), uint16 bf16 bits (dtype bf16) or uint8 e4m3 codes with
+    fp32 per-row scales x_scale [M] and w_scale [N] (dtype e4m3); b, gamma,
+    beta fp32."""
     rng = np.random.default_rng(seed)
     x = _normal(rng, (spec.M, spec.K), 1.0)
     W = _uniform(rng, (spec.N, spec.K), spec.w_bound)
@@ -151,6 +160,9 @@ def make_fgemm_inputs(spec, seed=0):
     out = {"b": b}
     if spec.dtype == "f32":
         out["x"], out["W"] = x, W
+    elif spec.dtype == "e4m3":
+        out["x"], out["x_scale"] = rows_to_e4m3(x)
+        out["W"], out["w_scale"] = rows_to_e4m3(W)
     else:
         out["x"], out["W"] = to_bf16_bits(x), to_bf16_bits(W)
     if spec.reduction == "groupnorm":

@@ -60,7 +60,8 @@ def test_plan_validation_statuses():
     assert plan_status(8, 256, 260, "bf16", "bf16", ok) == L.FG_ERR_ALIGNMENT  # K % 8
     assert plan_status(8, 256, 258, "f32", "f32", ok) == L.FG_ERR_ALIGNMENT    # K % 4
     assert plan_status(8, 252, 256, "bf16", "bf16", ok) == L.FG_ERR_ALIGNMENT  # N % 8 (bf16 out)
-    assert plan_status(8, 256, 256, "e4m3", "bf16", ok) == L.FG_ERR_UNSUPPORTED
+    assert plan_status(8, 256, 256, "e4m3", "bf16", ok) == L.FG_OK           # W8A8
+    assert plan_status(8, 256, 264, "e4m3", "bf16", ok) == L.FG_ERR_ALIGNMENT  # K % 16
     assert plan_status(8, 256, 256, 7, "bf16", ok) == L.FG_ERR_INVALID_ARG
     assert plan_status(8, 256, 256, "bf16", 9, ok) == L.FG_ERR_INVALID_ARG
     assert plan_status(8, 256, 256, "bf16", "bf16", None) == L.FG_ERR_INVALID_ARG
@@ -282,3 +283,16 @@ def test_finalize_and_rmsnorm_validation_on_the_host():
     with pytest.raises(L.FgError) as ei:
         L.add_rmsnorm(None, fake, fake, fake, 2, 16, 1e-5, None)
     assert ei.value.status == L.FG_ERR_INVALID_ARG
+
+
+def test_e4m3_run_needs_scales_on_the_host():
+    fake = 1 << 40
+    p = L.fgemm_plan(64, 256, 256, "e4m3", "bf16", E())
+    assert p.info()["tile_m"] in (128, 256)
+    for sx, sw in ((None, None), (fake, None), (None, fake)):
+        with pytest.raises(L.FgError) as ei:
+            L.fgemm_run_scaled(p, fake, fake, sx, sw, None, None, None, fake, None, 0)
+        assert ei.value.status == L.FG_ERR_INVALID_ARG
+    with pytest.raises(L.FgError) as ei:
+        L.fgemm_run(p, fake, fake, None, None, None, fake, None, 0)
+    assert ei.value.status == L.FG_ERR_INVALID_ARG and "scale" in L.last_error()

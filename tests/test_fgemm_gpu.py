@@ -12,11 +12,11 @@ import numpy as np
 import pytest
 import torch
 
-from oracle import bf16_decode, compare, ref_fgemm
+from oracle import bf16_decode, compare, e4m3_decode, ref_fgemm
 from paper_2606_02963_amd import api
 from paper_2606_02963_amd import _lib as L
 from paper_2606_02963_amd.synth import FGEMM_SPECS, FgemmSpec, make_fgemm_inputs
-from tests.gpu_helpers import dev_bf16, dev_f32, host64, log, require_gpu
+from tests.gpu_helpers import dev_bf16, dev_f32, dev_u8, host64, log, require_gpu
 
 pytestmark = pytest.mark.gpu
 
@@ -25,6 +25,12 @@ def _device_inputs(spec, inp):
     if spec.dtype == "f32":
         x, W = dev_f32(inp["x"]), dev_f32(inp["W"])
         x64, W64 = inp["x"].astype(np.float64), inp["W"].astype(np.float64)
+    elif spec.dtype == "e4m3":
+        # the oracle reads the exact values the fp8 MFMA multiplies: decoded
+        # codes times the per-row scales
+        x, W = dev_u8(inp["x"]), dev_u8(inp["W"])
+        x64 = e4m3_decode(inp["x"]) * inp["x_scale"].astype(np.float64)[:, None]
+        W64 = e4m3_decode(inp["W"]) * inp["w_scale"].astype(np.float64)[:, None]
     else:
         x, W = dev_bf16(inp["x"]), dev_bf16(inp["W"])
         x64, W64 = bf16_decode(inp["x"]), bf16_decode(inp["W"])
@@ -39,15 +45,18 @@ def run_spec(spec, seed=0, rows=None, inp=None, with_bias=True):
     log(f"[fgemm] {spec.name} M={spec.M} N={spec.N} K={spec.K} seed={seed}")
     inp = inp if inp is not None else make_fgemm_inputs(spec, seed)
     (x, W, b, g, be), (x64, W64) = _device_inputs(spec, inp)
+    sx = dev_f32(inp["x_scale"]) if spec.dtype == "e4m3" else None
+    sw = dev_f32(inp["w_scale"]) if spec.dtype == "e4m3" else None
     y = api.linear_epilogue(x, W, b if with_bias else None, spec.ops, spec.reduction, spec.gn_groups,
-                            spec.gn_eps, g, be, out_dtype=spec.out, post_ops=spec.post_ops)
+                            spec.gn_eps, g, be, out_dtype=spec.out, post_ops=spec.post_ops,
+                            x_scale=sx, w_scale=sw)
     torch.cuda.synchronize()
     got = host64(y)
     sel = slice(None) if rows is None else np.asarray(rows)
     ref = ref_fgemm(x64[sel], W64, inp["b"].astype(np.float64) if with_bias else None, spec.ops,
                     spec.reduction, spec.gn_groups, spec.gn_eps,
                     inp.get("gamma"), inp.get("beta"), spec.post_ops)
-    rep = compare(got[sel], ref, "f32" if spec.dtype == "f32" else "bf16")
+    rep = compare(got[sel], ref, {"f32": "f32", "bf16": "bf16", "e4m3": "e4m3"}[spec.dtype])
     log(f"    {rep}")
     assert rep.ok, f"{spec.name}: {rep}"
     return y
@@ -115,6 +124,44 @@ TABLE3 += [
 @pytest.mark.parametrize("spec", TABLE3, ids=lambda s: s.name)
 def test_parity_table3_chains(spec):
     run_spec(spec)
+
+
+# W8A8 (e4m3 codes, per-row fp32 scales): both e4m3 tiles, ragged M, N and
+# K tails (K = 272: two full 128-byte stages and a 16-byte tail), every
+# reduction, fp32 output.
+E8 = FGEMM_SPECS["e4m3_gelu_clamp"]
+E4M3 = [
+    E8.scaled(M=300, N=520, K=272),                    # 128×128 tiles, ragged, K tail
+    E8.scaled(M=1000, N=4104, K=1040),                 # 256×128 tiles, ragged, K tail
+    E8.scaled(M=2048, N=4096, K=512),                  # 256×128 tiles, full
+    FgemmSpec("e4m3_lse_mish", 300, 1000, 272, "e4m3", 1 / 16, (("scale", 2.0),), "lse",
+              post_ops=(("mish",),)),
+    FgemmSpec("e4m3_silu_gn", 520, 4096, 256, "e4m3", 1 / 16, (("silu",),), "groupnorm", 32, 1e-5),
+    FgemmSpec("e4m3_f32out", 130, 264, 208, "e4m3", 0.1, (("gelu_tanh",),), out_dtype="f32"),
+]
+
+
+@pytest.mark.parametrize("spec", E4M3, ids=lambda s: s.name)
+def test_parity_e4m3(spec):
+    run_spec(spec)
+
+
+def test_parity_e4m3_full_size_sampled_rows():
+    run_spec(E8, rows=[0, 1, 255, 256, 511, E8.M - 1])
+
+
+def test_e4m3_plan_needs_scales():
+    require_gpu()
+    spec = E8.scaled(M=64, N=128, K=64)
+    inp = make_fgemm_inputs(spec, 2)
+    x, W = dev_u8(inp["x"]), dev_u8(inp["W"])
+    plan = api.get_plan(spec.M, spec.N, spec.K, "e4m3", "bf16", False)
+    out = torch.empty((spec.M, spec.N), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(L.FgError) as ei:
+        L.fgemm_run(plan, x.data_ptr(), W.data_ptr(), None, None, None, out.data_ptr(), None, 0, None)
+    assert ei.value.status == L.FG_ERR_INVALID_ARG
+    with pytest.raises(ValueError):
+        api.linear_epilogue(x, W, None, ())
 
 
 @pytest.mark.parametrize("spec", T3, ids=lambda s: s.name)
