@@ -1,11 +1,13 @@
 // fg_tile.hpp — the tiled MFMA main loop shared by every GEMM in the library.
 //
-// One workgroup of WM × WN wave64s computes a BM × BN tile of acc = A·Bᵀ, where A rows and B rows are both contiguous along K (x rows and
-// nn.Linear weight rows). Per K stage each tile row contributes 128 bytes
-// (8 chunks of 16 B): 32 fp32, 64 bf16 or 128 e4m3 values. Stages are staged
-// HBM → VGPR → LDS with 128-bit loads and stores and double-buffered in LDS,
-// so the global loads of stage k+1 are in flight while stage k feeds the
-// matrix cores. Inside LDS each row's chunk c is stored at chunk
+// One workgroup of WM × WN wave64s computes a BM × BN tile of acc = A·Bᵀ,
+// where A rows and B rows are both contiguous along K (x rows and nn.Linear
+// weight rows). Per K stage each tile row contributes 128 bytes (8 chunks of
+// 16 B): 32 fp32, 64 bf16 or 128 e4m3 values. Stages go from memory straight
+// into LDS (buffer / global loads with the LDS bit, 16 bytes per lane) and
+// are double-buffered there, so the loads of stage k+1 are in flight while
+// stage k feeds the matrix cores (staging through VGPRs and 128-bit LDS
+// writes measured slower). Inside LDS each row's chunk c is stored at chunk
 // c ^ (row & 7) ^ ((row >> 3) & 1): a fragment read (16 consecutive rows, one
 // chunk) then touches sixteen distinct 16-byte bank groups of the 64-bank
 // LDS (rows alternate between its two 128-byte halves; the eight rows of one
