@@ -59,10 +59,17 @@ def parse():
 
 
 def kernel_source_hash(sources=KERNEL_SOURCES):
+    """Hash of the kernel sources with comments and whitespace removed, so
+    that committed counter summaries stay valid across comment edits but not
+    across code changes."""
+    import re
     h = hashlib.sha256()
     for f in sources:
-        with open(os.path.join(ROOT, "paper_2606_02963_amd", "csrc", f), "rb") as fh:
-            h.update(fh.read())
+        with open(os.path.join(ROOT, "paper_2606_02963_amd", "csrc", f), encoding="utf-8") as fh:
+            text = fh.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 
