@@ -296,3 +296,16 @@ def test_e4m3_run_needs_scales_on_the_host():
     with pytest.raises(L.FgError) as ei:
         L.fgemm_run(p, fake, fake, None, None, None, fake, None, 0)
     assert ei.value.status == L.FG_ERR_INVALID_ARG and "scale" in L.last_error()
+
+
+def test_header_is_plain_c():
+    # the boundary carries no C++ types: the header compiles as C99 (and C++)
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc")
+    if gcc is None:
+        pytest.skip("gcc not available")
+    for lang, std in (("c", "-std=c99"), ("c++", "-std=c++17")):
+        r = subprocess.run([gcc, std, "-Wall", "-Wextra", "-pedantic", "-Werror", "-fsyntax-only", "-x", lang,
+                            HEADER], capture_output=True, text=True)
+        assert r.returncode == 0, r.stderr
