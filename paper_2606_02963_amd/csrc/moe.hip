@@ -587,17 +587,22 @@ __global__ __launch_bounds__(256) void fill_i32_kernel(int32_t* p, int n, int v)
 // ---------------------------------------------------------------------------
 // host side
 
-// Prefill tiles are 128 × 128 (4 waves): on the T = 4096 step they measured
-// faster than 192- and 256-row tiles, whose ragged last m-tile per expert
-// (n_e ≈ 512 ± 22 slots) wastes more of the matrix cores.
+// Prefill tiles are 128 × 192 (4 waves, two workgroups per compute unit:
+// 2 × 80 KB of LDS rings fill the 160 KB). 192 weight rows per stage cut the
+// L2 → LDS bytes per FLOP by 17 % against 128 × 128 (13.0 vs 15.6 KB per
+// MFLOP, 52 vs 62.5 B/clk per compute unit at the full MFMA rate); 192- and
+// 256-row tiles lose more to the ragged last m-tile per
+// expert (n_e ≈ 512 ± 22 slots), and 128 × 256 fits one workgroup per unit.
+// Measured on the T = 4096 step: bf16 980–983 µs vs 1088–1090 µs with
+// 128 × 128, e4m3 697 vs 710–713 µs.
 // Decode e4m3 tiles are 192 weight rows wide: a tile then streams
 // 192 × H bytes, closer to the bf16 tile's 128 × 2H, so the per-tile start-up
 // is amortised over more bytes, and 192 divides the gpt-oss geometry exactly
 // (2880 = 30 × 96 h columns, 15 × 192 down rows). Measured: 161.8–162.2 µs vs
 // 165.1 µs for 128-row tiles and 177 µs for 256 on the T = 64 step.
-typedef Tile<In::BF16, 128, 128> GBf16Big;
+typedef Tile<In::BF16, 128, 192> GBf16Big;
 typedef Tile<In::BF16, 32, 128> GBf16Small;
-typedef Tile<In::E4M3, 128, 128> GF8Big;
+typedef Tile<In::E4M3, 128, 192> GF8Big;
 typedef Tile<In::E4M3, 32, 192> GF8Small;
 
 struct MoeLayout {
