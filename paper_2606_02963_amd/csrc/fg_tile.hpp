@@ -324,7 +324,13 @@ __device__ __forceinline__ void gemm_mainloop(const LA& ra, const LB& rb,
 
   Frag<TL> F0, F1;
   const int64_t KT = kbytes / TL::ROWB;   // full stages
+  if (KT > 0) {
+    ra.template stage<TL::NWAVES>(0, lds);
+    rb.template stage<TL::NWAVES>(0, lds + TL::BM * TL::ROWB);
+  }
   if (kbytes % TL::ROWB != 0) {
+    // the partial last stage goes through buffer 1 while stage 0 lands in
+    // buffer 0: both requests are in flight together
     char* sb = lds + TL::STAGE_BYTES;
     ra.template tail<TL::RSTRIDE>(KT * TL::ROWB, kbytes, sb);
     rb.template tail<TL::RSTRIDE>(KT * TL::ROWB, kbytes, sb + TL::BM * TL::ROWB);
@@ -337,8 +343,6 @@ __device__ __forceinline__ void gemm_mainloop(const LA& ra, const LB& rb,
     __syncthreads();
   }
   if (KT == 0) return;
-  ra.template stage<TL::NWAVES>(0, lds);
-  rb.template stage<TL::NWAVES>(0, lds + TL::BM * TL::ROWB);
   if (KT > 1) {
     char* s1 = lds + TL::STAGE_BYTES;
     ra.template stage<TL::NWAVES>(TL::ROWB, s1);
