@@ -57,6 +57,13 @@ def test_plan_validation_statuses():
     assert plan_status(-1, 256, 256, "bf16", "bf16", ok) == L.FG_ERR_INVALID_ARG
     assert plan_status(8, 0, 256, "bf16", "bf16", ok) == L.FG_ERR_INVALID_ARG
     assert plan_status(8, 256, 2 ** 31, "bf16", "bf16", ok) == L.FG_ERR_INVALID_ARG
+    # rows of at most 4 MiB: K = 2^21 bf16 / 2^22 e4m3 / 2^20 fp32, not one chunk more
+    assert plan_status(8, 256, 2 ** 21, "bf16", "bf16", ok) == L.FG_OK
+    assert plan_status(8, 256, 2 ** 21 + 8, "bf16", "bf16", ok) == L.FG_ERR_UNSUPPORTED
+    assert plan_status(8, 256, 2 ** 22, "e4m3", "bf16", ok) == L.FG_OK
+    assert plan_status(8, 256, 2 ** 22 + 16, "e4m3", "bf16", ok) == L.FG_ERR_UNSUPPORTED
+    assert plan_status(8, 256, 2 ** 20 + 4, "f32", "f32", ok) == L.FG_ERR_UNSUPPORTED
+    assert plan_status(2 ** 31 - 1, 8, 8, "bf16", "bf16", ok) == L.FG_OK      # M up to 2^31 - 1
     assert plan_status(8, 256, 260, "bf16", "bf16", ok) == L.FG_ERR_ALIGNMENT  # K % 8
     assert plan_status(8, 256, 258, "f32", "f32", ok) == L.FG_ERR_ALIGNMENT    # K % 4
     assert plan_status(8, 252, 256, "bf16", "bf16", ok) == L.FG_ERR_ALIGNMENT  # N % 8 (bf16 out)

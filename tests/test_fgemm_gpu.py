@@ -265,3 +265,40 @@ def test_split_k_ignores_workspace_contents_and_repeats_bit_identically():
     rep = compare(host64(outs[0])[rows], ref, "bf16")
     log(f"    {rep}")
     assert rep.ok, rep
+
+
+def test_x_and_y_past_4_gib():
+    """Maximum sizes along M: x and y each span more than 2^32 bytes
+    (540 000 rows of 4096 bf16), so tile base offsets and output row offsets
+    beyond 32 bits are exercised. x repeats a seeded 64-row block on the
+    device; each sampled output row is checked against the oracle row of its
+    block row (an output row depends only on its own input row)."""
+    require_gpu()
+    R, M = 64, 540_000
+    spec = C2.scaled(M=R, N=4096, K=4096)
+    inp = make_fgemm_inputs(spec, 11)
+    (blk, W, b, _, _), (x64, W64) = _device_inputs(spec, inp)
+    x = blk.repeat((M + R - 1) // R, 1)[:M]
+    assert x.is_contiguous() and x.numel() * 2 > 2 ** 32
+    log(f"[fgemm] offsets past 4 GiB M={M} N={spec.N} K={spec.K} "
+        f"{api.get_plan(M, spec.N, spec.K, 'bf16', 'bf16', True, spec.ops).info()}")
+    y = api.linear_epilogue(x, W, b, spec.ops)
+    torch.cuda.synchronize()
+    assert y.numel() * 2 > 2 ** 32
+    first_past = 2 ** 32 // (spec.K * 2)            # first row whose offset needs 33 bits
+    rows = np.array([0, 1, R - 1, 262_143, first_past - 1, first_past, first_past + 1, 530_001, M - 1])
+    got = host64(y[torch.from_numpy(rows).cuda()])
+    ref = ref_fgemm(x64, W64, inp["b"].astype(np.float64), spec.ops)[rows % R]
+    rep = compare(got, ref, "bf16")
+    log(f"    {rep}")
+    assert rep.ok, rep
+    del x, y
+
+
+@pytest.mark.parametrize("M,N,K", [(16, 16, 1 << 21), (40, 24, (1 << 21) - 8)])
+def test_k_at_the_row_limit(M, N, K):
+    """Maximum K: rows of 4 MiB (bf16 K = 2^21, the plan's limit), and one
+    8-element chunk short of it (a partial last stage), through split-K."""
+    spec = FgemmSpec(f"rowlimit_{K}", M, N, K, "bf16", 1 / 1024.0, C2.ops)
+    assert api.get_plan(M, N, K, "bf16", "bf16", True, spec.ops).info()["k_slices"] > 1
+    run_spec(spec, seed=12)
