@@ -232,3 +232,49 @@ def test_moe_validation_errors():
     with pytest.raises(L.FgError) as ei:
         L.moe_grouped_ffn(d, *([1 << 40] * 11), None, 0, None)
     assert ei.value.status == L.FG_ERR_WORKSPACE
+
+
+def test_moe_slots_past_4_gib():
+    """Maximum sizes: 190 000 tokens at top-4 give h and y_slot of more than
+    2^32 bytes (760 000 slot rows of 2880 bf16), so slot-row offsets past 32
+    bits are exercised in both grouped GEMMs and the finalize. Tokens and
+    logits repeat a seeded 64-token block on the device. Routing is checked
+    for every token against the block's oracle routing, the permutation and
+    offsets by their definition (numpy's stable argsort of the expert ids and
+    the exclusive prefix of their counts), and the outputs of sampled tokens,
+    including tokens whose h or y_slot rows lie past 4 GiB, against the
+    oracle."""
+    require_gpu()
+    R, T = 64, 190_000
+    spec = MoeSpec("slots_past_4gib", R)
+    act, w = make_moe_activations(spec, 21), make_moe_weights(spec, 21)
+    reps = (T + R - 1) // R
+    x = dev_bf16(act["x"]).repeat(reps, 1)[:T]
+    lg = dev_f32(act["logits"]).repeat(reps, 1)[:T]
+    wgu, wd, _, _ = _dev_weights(spec, w)
+    log(f"[moe] slots past 4 GiB T={T} H={spec.H} I={spec.I} E={spec.E} k={spec.k}")
+    res = api.moe_ffn(x, lg, wgu, wd, None, None, top_k=spec.k, alpha=spec.alpha, limit=spec.limit)
+    torch.cuda.synchronize()
+    S = T * spec.k
+    assert S * spec.I * 2 > 2 ** 32 and S * spec.H * 2 > 2 ** 32
+    ref = ref_moe(bf16_decode(act["x"]), act["logits"].astype(np.float64), _weights64(spec, w), spec.k,
+                  storage="bf16", act_quant=False, alpha=spec.alpha, limit=spec.limit, with_bound=True)
+    tok = np.arange(T) % R
+    idx = res.topk_idx.cpu().numpy()
+    assert np.array_equal(idx, ref["idx"][tok]), "top-k indices differ"
+    np.testing.assert_allclose(res.topk_w.cpu().numpy(), ref["w"][tok], rtol=1e-5, atol=0)
+    flat = idx.reshape(-1)
+    counts = np.bincount(flat, minlength=spec.E)
+    assert np.array_equal(res.offsets.cpu().numpy(), np.concatenate([[0], np.cumsum(counts)]))
+    perm = res.perm.cpu().numpy()
+    assert np.array_equal(perm, np.argsort(flat, kind="stable")), "permutation differs"
+    h_past = 2 ** 32 // (spec.I * 2)                     # first h row (expert order) needing 33 bits
+    y_past = 2 ** 32 // (spec.H * 2)                     # first y_slot row (slot order) needing 33 bits
+    h_late = np.unique(perm[h_past:] // spec.k)          # tokens with an h row past 4 GiB
+    y_late = y_past // spec.k + 1                        # a token whose y_slot rows are all past 4 GiB
+    sample = np.unique(np.concatenate([[0, 1, R - 1, 100_000, y_late, T - 2, T - 1],
+                                       h_late[:: max(1, h_late.size // 6)]]))
+    got = host64(res.out[torch.from_numpy(sample).cuda()])
+    rep = compare(got, ref["out"][sample % R], "bf16", slack=ref["out_bound"][sample % R])
+    log(f"    {sample.size} sampled tokens: {rep}")
+    assert rep.ok, rep
