@@ -650,9 +650,9 @@ def bench_rope_kv(args, torch, np):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1",
+        print(json.dumps({"error": "the library runs one GPU per process and has no multi-GPU path; --gpus must be 1",
                           "n_gpus": args.gpus}))
-        print("bench.py: multi-GPU runs are not part of this build (one GPU per box); use --gpus 1",
+        print("bench.py: no multi-GPU path is implemented (the step runs on one GPU); use --gpus 1",
               file=sys.stderr)
         sys.exit(2)
 

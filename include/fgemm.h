@@ -54,7 +54,7 @@ extern "C" {
 typedef enum {
   FG_OK = 0,
   FG_ERR_INVALID_ARG = 1,   /* null pointer, bad shape, bad enum value */
-  FG_ERR_UNSUPPORTED = 2,   /* valid request this build has no kernel for */
+  FG_ERR_UNSUPPORTED = 2,   /* valid request the library has no kernel for */
   FG_ERR_ALIGNMENT = 3,     /* pointer or leading dimension not aligned */
   FG_ERR_WORKSPACE = 4,     /* workspace missing or smaller than required */
   FG_ERR_HIP = 5            /* the HIP runtime reported a launch error */
