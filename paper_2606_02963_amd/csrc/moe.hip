@@ -20,6 +20,8 @@
 #include <hip/hip_runtime.h>
 #include <math.h>
 
+#include <atomic>
+
 #include "fg_host.hpp"
 #include "fg_quant.hpp"
 #include "fg_tile.hpp"
@@ -673,25 +675,30 @@ static fg_status validate_desc(const moe_desc* d, const char* fn) {
   return FG_OK;
 }
 
-// n-tiles: gate/up tiles cover BN/2 columns of h (BN weight rows, gate and
-// up interleaved), down tiles BN columns of the output.
 // Resident workgroups of a kernel on the current device (occupancy × CUs),
-// queried once per kernel and device.
+// queried once per kernel and device. Concurrent first calls from several
+// host threads compute the same value; the relaxed atomics keep that free
+// of data races.
 template <class TL, int EPI>
 static int resident_workgroups() {
-  static int cached[64] = {0};
+  static std::atomic<int> cached[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cached[dev] == 0) {
+  int v = cached[dev].load(std::memory_order_relaxed);
+  if (v == 0) {
     int per_cu = 0, cus = 0;
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, grouped_kernel<TL, EPI>, TL::THREADS, 0) != hipSuccess ||
         per_cu < 1)
       per_cu = 1;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) cus = 256;
-    cached[dev] = per_cu * cus;
+    v = per_cu * cus;
+    cached[dev].store(v, std::memory_order_relaxed);
   }
-  return cached[dev];
+  return v;
 }
+
+// n-tiles: gate/up tiles cover BN/2 columns of h (BN weight rows, gate and
+// up interleaved), down tiles BN columns of the output.
 
 template <class TL, int EPI>
 static void launch_grouped(GroupedArgs a, int64_t S, hipStream_t s) {
