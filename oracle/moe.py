@@ -26,9 +26,11 @@ The oracle takes the block's steps in order, each as its plain definition:
             h is stored in the method's declared intermediate format,
             modelled here: bf16 RNE; in the W8A8 variant the bf16 h is
             then quantised per row to e4m3 with an fp32 scale;
-            y_slot[rows] = h·W_d[e]ᵀ, multiplied by the routing weight of
-            each slot and stored as bf16 (RNE), the method's declared format
-  finalize  out[t] = Σ_j y_slot[t·k + j], j ascending
+            y_slot[rows] = h·W_d[e]ᵀ
+  finalize  out[t] = Σ_j w[t, j]·y_slot[t·k + j], j ascending: the
+            routing-weighted sum, kept exact (fp64) until the single output
+            rounding, which the comparison applies to nothing (the oracle
+            output is returned unrounded)
 
 fp8 (W8A8) variant: weights are stored as e4m3 codes with one fp32 scale per
 output row (decoded before they reach this oracle); activations (x per
@@ -106,6 +108,22 @@ def _bf16(v):
     return bf16_decode(bf16_encode_rne(v))
 
 
+def store_h(h, storage):
+    """The declared storage of the intermediate h (the down GEMM's operand):
+    "bf16" rounds to bf16 (RNE); "e4m3" rounds to bf16 and then quantises
+    each row to e4m3 codes with an fp32 scale (decoded back to values);
+    "none" keeps h exact."""
+    if storage == "none":
+        return h
+    hb = bf16_decode(bf16_encode_rne(h))
+    if storage == "bf16":
+        return hb
+    if storage == "e4m3":
+        q, s = ref_quant_rows_e4m3(hb)
+        return _dequant_rows(q, s)
+    raise ValueError(f"unknown storage {storage!r}")
+
+
 # Relative and row-absolute size of the neighbourhood of a storage rounding
 # boundary inside which a kernel that evaluates h in fp32 (a different
 # rounding order than this fp64 oracle) may legitimately take the other
@@ -119,18 +137,17 @@ def storage_deviation(h, storage):
     """Largest change of the stored value of each element of h (per row for
     the per-row-scaled e4m3 storage) over the rounding decisions that are
     within FRAGILE_REL·|h| + FRAGILE_ABS·max|h_row| of a boundary. Zero for
-    every element whose stored value is robust. Returns (stored, deviation)."""
+    every element whose stored value is robust. Returns (stored, deviation),
+    stored being store_h(h, storage)."""
     h = np.asarray(h, dtype=np.float64)
-    pert = FRAGILE_REL * np.abs(h) + FRAGILE_ABS * np.max(np.abs(h), axis=-1, keepdims=True)
+    stored = store_h(h, storage)
     if storage == "none":
-        return h, np.zeros_like(h)
+        return stored, np.zeros_like(h)
+    pert = FRAGILE_REL * np.abs(h) + FRAGILE_ABS * np.max(np.abs(h), axis=-1, keepdims=True)
     b_ref, b_lo, b_hi = _bf16(h), _bf16(h - pert), _bf16(h + pert)
     if storage == "bf16":
-        return b_ref, np.maximum(np.abs(b_lo - b_ref), np.abs(b_hi - b_ref))
-    if storage != "e4m3":
-        raise ValueError(f"unknown storage {storage!r}")
-    q, s_ref = ref_quant_rows_e4m3(b_ref)
-    stored = _dequant_rows(q, s_ref)
+        return stored, np.maximum(np.abs(b_lo - b_ref), np.abs(b_hi - b_ref))
+    s_ref = ref_quant_rows_e4m3(b_ref)[1]
     scales = [s_ref, ref_quant_rows_e4m3(b_lo)[1], ref_quant_rows_e4m3(b_hi)[1]]
     dev = np.zeros_like(h)
     for b in (b_ref, b_lo, b_hi):
@@ -180,18 +197,11 @@ def ref_expert_rows(X, W_gu, W_d, storage="bf16", act_quant=False, alpha=1.702,
     if with_bound:
         h, dev = storage_deviation(h, storage)
         return h @ W_d.T, dev @ np.abs(W_d).T
-    if storage == "bf16":
-        h = bf16_decode(bf16_encode_rne(h))
-    elif storage == "e4m3":
-        q, s = ref_quant_rows_e4m3(bf16_decode(bf16_encode_rne(h)))
-        h = _dequant_rows(q, s)
-    elif storage != "none":
-        raise ValueError(f"unknown storage {storage!r}")
-    return h @ W_d.T
+    return store_h(h, storage) @ W_d.T
 
 
 def ref_moe(x, logits, weights, k, storage="bf16", act_quant=False, alpha=1.702,
-            limit=7.0, interleaved=False, tokens=None, with_bound=False, slot_storage="bf16"):
+            limit=7.0, interleaved=False, tokens=None, with_bound=False):
     """The MoE expert FFN step, fp64.
 
     x: [T, H] fp64 (decoded bf16 tokens); logits: [T, E] (fp32 values);
@@ -199,8 +209,6 @@ def ref_moe(x, logits, weights, k, storage="bf16", act_quant=False, alpha=1.702,
     applied), or a pair of arrays [E, 2I, H], [E, H, I].
     tokens: optional subset of token ids whose outputs to compute (a token's
     output depends only on its own row and its own routing).
-    slot_storage: "bf16" (the routing-weighted slot outputs are stored as
-    bf16 before the finalize sum, as the method declares) or "none".
     with_bound: also return "out_bound", per output element the largest
     change any storage-rounding decision of h within the fragile
     neighbourhood of a boundary (see storage_deviation) can cause; a kernel
@@ -238,25 +246,14 @@ def ref_moe(x, logits, weights, k, storage="bf16", act_quant=False, alpha=1.702,
             y = ref_expert_rows(x[slots // k], W_gu, W_d, storage, act_quant, alpha,
                                 limit, interleaved)
         y_slot[dst] = y
-    # the routing weight is applied per slot and the weighted slot output is
-    # stored as bf16; finalize sums the k stored slots of each token, j ascending
+    # finalize: the routing-weighted sum of each token's k slot outputs,
+    # j ascending, exact until the output
     out = np.zeros((tok.size, H), dtype=np.float64)
     bound = np.zeros((tok.size, H), dtype=np.float64) if with_bound else None
     for j in range(k):
-        ys = w[tok, j][:, None] * y_slot[j::k]
-        if slot_storage == "bf16":
-            stored = bf16_decode(bf16_encode_rne(ys))
-            if with_bound:
-                # either neighbouring bf16 value is a legitimate rounding of ys
-                # when ys moves within its own bound plus fp32 evaluation noise
-                yb = w[tok, j][:, None] * b_slot[j::k] + FRAGILE_REL * np.abs(ys)
-                lo = bf16_decode(bf16_encode_rne(ys - yb))
-                hi = bf16_decode(bf16_encode_rne(ys + yb))
-                bound += np.maximum(np.abs(lo - stored), np.abs(hi - stored))
-            ys = stored
-        elif with_bound:
+        out += w[tok, j][:, None] * y_slot[j::k]
+        if with_bound:
             bound += w[tok, j][:, None] * b_slot[j::k]
-        out += ys
     res = {"out": out, "idx": idx, "w": w, "counts": counts, "offsets": offsets, "perm": perm}
     if with_bound:
         res["out_bound"] = bound

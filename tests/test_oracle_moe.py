@@ -7,7 +7,12 @@ forms (arange and all-equal logits); the permutation against its definition
 mpmath; the whole block against a token-order brute force in mpmath that
 never builds the permutation, against the dense FFN it reduces to at E = 1,
 k = 1, and against the identical-experts and zero-W_down closed forms. The
-fp8 activation quantiser is pinned by the e4m3 grid and by its extreme code.
+W8A8 composition (per-token and per-slot-row e4m3 quantisation, e4m3
+weights with per-row scales) is pinned by a second token-order brute force
+that rebuilds every storage rounding from the format definitions with exact
+rationals, and planted mistakes in the dequantisation and in h's storage
+must fail it. The fp8 activation quantiser is pinned by the e4m3 grid and by
+its extreme code.
 The standalone finalize is pinned by an mpmath brute force over (token,
 column, slot), the k = 1 identity and an exactly cancelling slot pair."""
 
@@ -130,9 +135,7 @@ def _mp_bruteforce_moe(x, lg, Wgu, Wd, k, alpha=1.702, limit=7.0):
                 h.append(mp.mpf(float(bf16_decode(bf16_encode_rne(np.array([float(hv)])))[0])))
             for n in range(H):
                 y = mp.fsum(h[i] * mp.mpf(float(Wd[e, n, i])) for i in range(I))
-                # the routing-weighted slot output is stored as bf16 before the sum
-                ys = float(bf16_decode(bf16_encode_rne(np.array([float(ex[j] / den * y)])))[0])
-                acc[n] += mp.mpf(ys)
+                acc[n] += ex[j] / den * y
         out[t] = [float(v) for v in acc]
     return out
 
@@ -159,8 +162,7 @@ def test_moe_single_expert_is_dense_ffn():
     x = rng.standard_normal((T, H))
     Wgu = rng.standard_normal((1, 2 * I, H)) * 0.5
     Wd = rng.standard_normal((1, H, I)) * 0.5
-    got = ref_moe(x, rng.standard_normal((T, 1)), (Wgu, Wd), 1, storage="none",
-                  slot_storage="none")["out"]
+    got = ref_moe(x, rng.standard_normal((T, 1)), (Wgu, Wd), 1, storage="none")["out"]
     G = ref_fgemm(x, Wgu[0])
     h = ref_swiglu_clamped(G[:, :I], G[:, I:])
     np.testing.assert_allclose(got, ref_fgemm(h, Wd[0]), rtol=1e-14, atol=1e-14)
@@ -175,7 +177,7 @@ def test_moe_identical_experts_and_zero_down():
     Wgu = np.stack([wgu1] * E)
     Wd = np.stack([wd1] * E)
     lg = rng.standard_normal((T, E))
-    got = ref_moe(x, lg, (Wgu, Wd), 3, storage="none", slot_storage="none")["out"]
+    got = ref_moe(x, lg, (Wgu, Wd), 3, storage="none")["out"]
     G = x @ wgu1.T
     want = ref_swiglu_clamped(G[:, :I], G[:, I:]) @ wd1.T
     np.testing.assert_allclose(got, want, rtol=1e-13, atol=1e-13)
@@ -190,10 +192,10 @@ def test_interleaved_gate_up_is_a_row_permutation():
     Wgu = rng.standard_normal((1, 2 * I, H))
     Wd = rng.standard_normal((1, H, I))
     lg = np.zeros((T, 1))
-    a = ref_moe(x, lg, (Wgu, Wd), 1, storage="none", slot_storage="none")["out"]
+    a = ref_moe(x, lg, (Wgu, Wd), 1, storage="none")["out"]
     inter = np.empty_like(Wgu)
     inter[0, 0::2], inter[0, 1::2] = Wgu[0, :I], Wgu[0, I:]
-    b = ref_moe(x, lg, (inter, Wd), 1, storage="none", interleaved=True, slot_storage="none")["out"]
+    b = ref_moe(x, lg, (inter, Wd), 1, storage="none", interleaved=True)["out"]
     np.testing.assert_allclose(a, b, rtol=1e-15, atol=1e-15)
 
 
@@ -306,8 +308,7 @@ def test_storage_deviation_bound():
     x = rng.standard_normal((6, 8))
     Wgu = rng.standard_normal((2, 8, 8)) * 0.3
     Wd = rng.standard_normal((2, 8, 4)) * 0.3
-    r = ref_moe(x, rng.standard_normal((6, 2)), (Wgu, Wd), 2, storage="none", with_bound=True,
-                slot_storage="none")
+    r = ref_moe(x, rng.standard_normal((6, 2)), (Wgu, Wd), 2, storage="none", with_bound=True)
     assert np.all(r["out_bound"] == 0.0)
     r2 = ref_moe(x, rng.standard_normal((6, 2)), (Wgu, Wd), 2, storage="e4m3", with_bound=True)
     assert np.all(r2["out_bound"] >= 0.0)
@@ -350,3 +351,164 @@ def test_finalize_planted_stride_mistake_is_caught():
     with pytest.raises(AssertionError):
         test_finalize_bruteforce_via(wrong_stride)
 
+
+
+# ---------------------------------------------------------------------------
+# W8A8 (e4m3) MoE path. The brute force below rebuilds every storage step from
+# the format definitions with exact rationals, sharing nothing with
+# ``oracle.codecs`` or ``oracle.moe``'s quantiser: OCP e4m3fn values
+# (−1)^s·2^(e−7)·(1 + f/8), subnormals 2^−6·f/8, largest finite 448, rounded
+# to nearest with ties to the even code and saturated; bf16 values rounded to
+# 8 significant bits, ties to even; the per-row scale fp32(amax/448) (1 for a
+# zero row) and the quotient fp32(v/s) taken in fp32 (numpy float32
+# arithmetic is IEEE binary32 with correct rounding), the precision in which
+# the method takes those decisions.
+
+from fractions import Fraction
+
+_E4M3_POS = [Fraction(c & 7, 8) * Fraction(2) ** -6 if (c >> 3) == 0
+             else (1 + Fraction(c & 7, 8)) * Fraction(2) ** ((c >> 3) - 7) for c in range(0x7F)]
+assert _E4M3_POS[-1] == 448
+
+
+def _frac(v):
+    if isinstance(v, mp.mpf):
+        man, exp = v.man_exp                      # |mantissa| and exponent; the sign is separate
+        return (-1 if v < 0 else 1) * Fraction(int(man)) * Fraction(2) ** int(exp)
+    return Fraction(float(v))
+
+
+def _e4m3_round(v):
+    """Nearest e4m3fn value to v (exact rational), ties to the even code,
+    magnitudes past 448 saturated."""
+    a = abs(_frac(v))
+    sign = -1 if _frac(v) < 0 else 1
+    if a >= 448:
+        return sign * Fraction(448)
+    lo = max(c for c in range(0x7F) if _E4M3_POS[c] <= a)
+    if _E4M3_POS[lo] == a:
+        return sign * a
+    hi = lo + 1
+    dl, dh = a - _E4M3_POS[lo], _E4M3_POS[hi] - a
+    c = lo if dl < dh else hi if dh < dl else (lo if lo % 2 == 0 else hi)
+    return sign * _E4M3_POS[c]
+
+
+def _bf16_round(v):
+    """Nearest bf16 value (8 significant bits, ties to even) to v, normal range."""
+    a = abs(_frac(v))
+    if a == 0:
+        return Fraction(0)
+    e = a.numerator.bit_length() - a.denominator.bit_length()
+    if Fraction(2) ** e > a:
+        e -= 1
+    ulp = Fraction(2) ** (e - 7)
+    q = a / ulp
+    n = q.numerator // q.denominator
+    r = q - n
+    if r > Fraction(1, 2) or (r == Fraction(1, 2) and n % 2 == 1):
+        n += 1
+    return (-1 if _frac(v) < 0 else 1) * n * ulp
+
+
+def _row_quant(vals):
+    """Per-row e4m3 storage of exact values that are fp32-representable:
+    s = fp32(amax/448) (1 for a zero row), value_i = e4m3(fp32(v_i/s))·s."""
+    f32 = [np.float32(float(v)) for v in vals]
+    assert all(Fraction(float(a)) == _frac(v) for a, v in zip(f32, vals))   # exact in fp32
+    amax = max(abs(a) for a in f32)
+    s = np.float32(1.0) if amax == 0 else np.float32(amax) / np.float32(448.0)
+    return [_e4m3_round(np.float32(a) / s) * Fraction(float(s)) for a in f32]
+
+
+def _mp(fr):
+    fr = Fraction(fr)
+    return mp.mpf(fr.numerator) / fr.denominator
+
+
+def _e4m3_decode_def(code):
+    code = int(code)
+    v = _E4M3_POS[code & 0x7F]
+    return -v if code & 0x80 else v
+
+
+def _mp_bruteforce_moe_w8a8(x, lg, gu_codes, gu_s, d_codes, d_s, k, alpha=1.702, limit=7.0):
+    T, H = x.shape
+    E = lg.shape[1]
+    I = d_codes.shape[2]
+    Wgu = [[[_mp(_e4m3_decode_def(gu_codes[e, n, c]) * Fraction(float(gu_s[e, n]))) for c in range(H)]
+            for n in range(2 * I)] for e in range(E)]
+    Wd = [[[_mp(_e4m3_decode_def(d_codes[e, n, i]) * Fraction(float(d_s[e, n]))) for i in range(I)]
+           for n in range(H)] for e in range(E)]
+    out = np.zeros((T, H))
+    for t in range(T):
+        order = sorted(range(E), key=lambda e: (-lg[t, e], e))[:k]
+        ex = [mp.exp(mp.mpf(float(lg[t, e]))) for e in order]
+        den = mp.fsum(ex)
+        xq = [_mp(v) for v in _row_quant([float(v) for v in x[t]])]
+        acc = [mp.mpf(0)] * H
+        for j, e in enumerate(order):
+            G = [mp.fsum(xq[c] * Wgu[e][n][c] for c in range(H)) for n in range(2 * I)]
+            hb = []
+            for i in range(I):
+                g = min(G[i], limit)
+                u = min(max(G[I + i], -limit), limit)
+                hb.append(_bf16_round((u + 1) * g / (1 + mp.exp(-mp.mpf(alpha) * g))))
+            hq = [_mp(v) for v in _row_quant(hb)]
+            for n in range(H):
+                acc[n] += ex[j] / den * mp.fsum(hq[i] * Wd[e][n][i] for i in range(I))
+        out[t] = [float(v) for v in acc]
+    return out
+
+
+def _w8a8_case():
+    spec = MoeSpec("w8a8_pin", T=3, H=64, I=64, E=2, k=2, w_dtype="e4m3", w_std=0.15)
+    act, w = make_moe_activations(spec, 5), make_moe_weights(spec, 5)
+    x = bf16_decode(act["x"])
+    lg = act["logits"].astype(np.float64)
+    return spec, x, lg, w
+
+
+def _w8a8_weights64(w):
+    return lambda e: (e4m3_decode(w["w_gate_up"][e]) * w["s_gate_up"][e][:, None].astype(np.float64),
+                      e4m3_decode(w["w_down"][e]) * w["s_down"][e][:, None].astype(np.float64))
+
+
+_W8A8_WANT = {}
+
+
+def test_moe_w8a8_bruteforce_token_order():
+    """The W8A8 composition (tokens quantised per row, bf16 h quantised per
+    slot row, e4m3 weights with per-row scales) against the definition-level
+    brute force, through both oracle paths (plain and with the flip bound).
+    The weight scales and the activation scales are all far from 1."""
+    spec, x, lg, w = _w8a8_case()
+    assert np.all(np.abs(np.log2(w["s_gate_up"])) > 4) and np.all(np.abs(np.log2(w["s_down"])) > 4)
+    if "want" not in _W8A8_WANT:
+        _W8A8_WANT["want"] = _mp_bruteforce_moe_w8a8(x, lg, w["w_gate_up"], w["s_gate_up"], w["w_down"],
+                                                     w["s_down"], spec.k)
+    want = _W8A8_WANT["want"]
+    for bound in (False, True):
+        got = ref_moe(x, lg, _w8a8_weights64(w), spec.k, storage="e4m3", act_quant=True,
+                      with_bound=bound)["out"]
+        np.testing.assert_allclose(got, want, rtol=1e-12, atol=1e-12 * np.max(np.abs(want)))
+
+
+def test_moe_w8a8_planted_mistakes_are_caught(monkeypatch):
+    """A division in place of the multiplication by the row scale when the
+    e4m3 codes are decoded, and h quantised straight from its exact value
+    without the bf16 storage step, each fail the W8A8 brute-force pin."""
+    def dequant_divides(codes, s):
+        return e4m3_decode(codes) / np.asarray(s, dtype=np.float64)[..., None]
+
+    def store_h_without_bf16(h, storage):
+        if storage == "e4m3":
+            q, s = ref_quant_rows_e4m3(h)
+            return om._dequant_rows(q, s)
+        return orig_store(h, storage)
+    orig_store = om.store_h
+    for name, fake in (("_dequant_rows", dequant_divides), ("store_h", store_h_without_bf16)):
+        with monkeypatch.context() as m:
+            m.setattr(om, name, fake)
+            with pytest.raises(AssertionError):
+                test_moe_w8a8_bruteforce_token_order()
