@@ -317,6 +317,28 @@ fg_status bias_rope_kv_update(const rope_desc *d, const void *qkv, const void *b
 fg_status fg_quantize_rows_e4m3(const void *x, int64_t rows, int64_t cols,
                                 uint8_t *q, float *s, void *stream);
 
+/*
+ * Launch trace, for benchmarks and measurement tools. fg_trace_begin opens a
+ * trace on the calling thread: from then on, the i-th kernel launch that any
+ * entry point makes on this thread (i < capacity; later launches are not
+ * traced) records one HIP event right before and one right after the
+ * launch, on the launch's stream. fg_trace_end closes the trace and returns
+ * the number of launches traced. fg_trace_read(i, ms, kernel) then waits
+ * for launch i's second event and gives the time between its two events in
+ * milliseconds, and the kernel's symbol name as the HIP runtime reports it
+ * (valid until the next trace); either output may be NULL. The events are
+ * created by the library on first use and kept for the thread's later
+ * traces. While a trace is open, event records are enqueued beside every
+ * launch, so a trace must not be open during graph capture and the timings
+ * of untraced runs are the reference for throughput.
+ * FG_ERR_INVALID_ARG for a capacity outside 1 .. 2^20, a read while the
+ * trace is open or an index outside the traced launches; FG_ERR_HIP if the
+ * runtime fails to create, wait for or time an event.
+ */
+fg_status fg_trace_begin(int32_t capacity);
+int32_t fg_trace_end(void);
+fg_status fg_trace_read(int32_t i, float *ms, const char **kernel);
+
 /* Static description of a status code. */
 const char *fg_status_str(fg_status s);
 

@@ -147,12 +147,25 @@ def storage_deviation(h, storage):
     b_ref, b_lo, b_hi = _bf16(h), _bf16(h - pert), _bf16(h + pert)
     if storage == "bf16":
         return stored, np.maximum(np.abs(b_lo - b_ref), np.abs(b_hi - b_ref))
-    s_ref = ref_quant_rows_e4m3(b_ref)[1]
-    scales = [s_ref, ref_quant_rows_e4m3(b_lo)[1], ref_quant_rows_e4m3(b_hi)[1]]
+    # the e4m3 decision of a bf16 value under a given scale is taken in fp32
+    # on both sides, so only the bf16 decisions (of each element, and of the
+    # row maximum, which sets the scale) can go either way
+    bs = (b_ref, b_lo, b_hi)
+    scales = [ref_quant_rows_e4m3(b)[1] for b in bs]
     dev = np.zeros_like(h)
-    for b in (b_ref, b_lo, b_hi):
+    # rows whose scale is fragile: every combination of element and scale decisions
+    rows = np.flatnonzero((scales[1] != scales[0]) | (scales[2] != scales[0]))
+    for b in bs:
         for sc in scales:
-            dev = np.maximum(dev, np.abs(_dequant_with_scale(b, sc) - stored))
+            dev[rows] = np.maximum(dev[rows], np.abs(_dequant_with_scale(b[rows], sc[rows]) - stored[rows]))
+    # the other rows keep their scale: only elements whose bf16 value may differ can move
+    keep = np.ones(h.shape[0], dtype=bool)
+    keep[rows] = False
+    for b in (b_lo, b_hi):
+        r, c = np.nonzero((b != b_ref) & keep[:, None])
+        sc = scales[0][r]
+        moved = e4m3_decode(e4m3_encode_rne_sat(f32_round(f32_round(b[r, c]) / sc))) * sc
+        dev[r, c] = np.maximum(dev[r, c], np.abs(moved - stored[r, c]))
     return stored, dev
 
 

@@ -89,6 +89,12 @@ def lib():
         L.bias_rope_kv_update.restype = i32
         L.fg_quantize_rows_e4m3.argtypes = [vp, i64, i64, vp, vp, vp]
         L.fg_quantize_rows_e4m3.restype = i32
+        L.fg_trace_begin.argtypes = [i32]
+        L.fg_trace_begin.restype = i32
+        L.fg_trace_end.argtypes = []
+        L.fg_trace_end.restype = i32
+        L.fg_trace_read.argtypes = [i32, C.POINTER(C.c_float), C.POINTER(C.c_char_p)]
+        L.fg_trace_read.restype = i32
         L.fg_status_str.argtypes = [i32]
         L.fg_status_str.restype = C.c_char_p
         L.fg_last_error.argtypes = []
@@ -216,6 +222,21 @@ def moe_grouped_ffn(desc, tokens, router_logits, w_gateup, w_down, s_gateup, s_d
 
 def fg_quantize_rows_e4m3(x, rows, cols, q, s, stream=None):
     _check(lib().fg_quantize_rows_e4m3(x, int(rows), int(cols), q, s, stream), "fg_quantize_rows_e4m3")
+
+
+def fg_trace_begin(capacity):
+    _check(lib().fg_trace_begin(int(capacity)), "fg_trace_begin")
+
+
+def fg_trace_end():
+    return lib().fg_trace_end()
+
+
+def fg_trace_read(i):
+    """(milliseconds between the two events of traced launch i, kernel name)."""
+    ms, name = C.c_float(), C.c_char_p()
+    _check(lib().fg_trace_read(int(i), C.byref(ms), C.byref(name)), "fg_trace_read")
+    return ms.value, (name.value or b"").decode(errors="replace")
 
 
 def moe_finalize(y_slot, out, T, H, top_k, stream=None):

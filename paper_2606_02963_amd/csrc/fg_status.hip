@@ -3,6 +3,8 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <vector>
+
 #include "fg_host.hpp"
 #include "fgemm.h"
 
@@ -20,13 +22,84 @@ fg_status fail(fg_status st, const char* fmt, ...) {
 
 void clear_error() { g_last_error[0] = '\0'; }
 
-fg_status check_launch(const char* what) {
-  const hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return fail(FG_ERR_HIP, "%s: kernel launch failed: %s", what, hipGetErrorString(e));
-  return FG_OK;
+fg_status check_launch(const char* what, const Launches& l) {
+  if (l.first == hipSuccess) return FG_OK;
+  (void)hipGetLastError();
+  return fail(FG_ERR_HIP, "%s: kernel launch failed: %s", what, hipGetErrorString(l.first));
+}
+
+// The open launch trace of a thread: two events per launch slot, created
+// on first use and kept for the thread's later traces.
+struct TraceState {
+  std::vector<hipEvent_t> ev;
+  std::vector<const void*> kernel;
+  int cap = 0, n = 0;
+  bool open = false;
+};
+static thread_local TraceState g_trace;
+
+int trace_launch_begin(hipStream_t s) {
+  TraceState& t = g_trace;
+  if (!t.open || t.n >= t.cap) return -1;
+  const int i = t.n++;
+  (void)hipEventRecord(t.ev[2 * i], s);
+  return i;
+}
+
+void trace_launch_end(int slot, hipStream_t s, const void* kernel) {
+  g_trace.kernel[slot] = kernel;
+  (void)hipEventRecord(g_trace.ev[2 * slot + 1], s);
 }
 
 }  // namespace fg
+
+extern "C" fg_status fg_trace_begin(int32_t capacity) {
+  using namespace fg;
+  clear_error();
+  TraceState& t = g_trace;
+  if (capacity < 1 || capacity > (1 << 20))
+    return fail(FG_ERR_INVALID_ARG, "fg_trace_begin: capacity %d outside 1..2^20", capacity);
+  while ((int64_t)t.ev.size() < 2 * (int64_t)capacity) {
+    hipEvent_t e;
+    const hipError_t err = hipEventCreate(&e);
+    if (err != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(FG_ERR_HIP, "fg_trace_begin: hipEventCreate failed: %s", hipGetErrorString(err));
+    }
+    t.ev.push_back(e);
+  }
+  t.kernel.assign(capacity, nullptr);
+  t.cap = capacity;
+  t.n = 0;
+  t.open = true;
+  return FG_OK;
+}
+
+extern "C" int32_t fg_trace_end(void) {
+  fg::g_trace.open = false;
+  return fg::g_trace.n;
+}
+
+extern "C" fg_status fg_trace_read(int32_t i, float* ms, const char** kernel) {
+  using namespace fg;
+  clear_error();
+  TraceState& t = g_trace;
+  if (t.open) return fail(FG_ERR_INVALID_ARG, "fg_trace_read: the trace is still open");
+  if (i < 0 || i >= t.n) return fail(FG_ERR_INVALID_ARG, "fg_trace_read: launch %d outside 0..%d", i, t.n - 1);
+  if (ms != nullptr) {
+    hipError_t err = hipEventSynchronize(t.ev[2 * i + 1]);
+    if (err == hipSuccess) err = hipEventElapsedTime(ms, t.ev[2 * i], t.ev[2 * i + 1]);
+    if (err != hipSuccess) {
+      (void)hipGetLastError();
+      return fail(FG_ERR_HIP, "fg_trace_read: %s", hipGetErrorString(err));
+    }
+  }
+  if (kernel != nullptr) {
+    const char* name = hipKernelNameRefByPtr(t.kernel[i], nullptr);
+    *kernel = name != nullptr ? name : "";
+  }
+  return FG_OK;
+}
 
 extern "C" const char* fg_status_str(fg_status s) {
   switch (s) {

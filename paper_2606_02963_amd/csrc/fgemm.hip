@@ -592,13 +592,14 @@ static fg_status run_plan(const fg_plan* plan, const void* A, const void* W, con
   if (kc.fn == nullptr) return fail(FG_ERR_UNSUPPORTED, "fgemm_run: no kernel for this plan");
   hipStream_t s = static_cast<hipStream_t>(stream);
   const unsigned grid = (unsigned)(p.tiles_m * p.tiles_n * p.ks);
-  hipLaunchKernelGGL(kc.fn, dim3(grid), dim3(kc.threads), 0, s, a, ep, post);
+  Launches lc;
+  lc.add(launch(kc.fn, dim3(grid), dim3(kc.threads), 0, s, a, ep, post));
   if (red == FG_RED_LOGSUMEXP_ROW) {
     const unsigned g2 = (unsigned)((p.M + 3) / 4);
-    hipLaunchKernelGGL(lse_combine_kernel, dim3(g2), dim3(256), 0, s, a.ws, static_cast<float*>(out),
-                       (int)p.M, (int)p.tiles_n, post);
+    lc.add(launch(lse_combine_kernel, dim3(g2), dim3(256), 0, s, a.ws, static_cast<float*>(out), (int)p.M,
+                  (int)p.tiles_n, post));
   }
-  return check_launch("fgemm_run");
+  return check_launch("fgemm_run", lc);
 }
 
 extern "C" fg_status fgemm_run(const fg_plan* plan, const void* A, const void* W, const float* bias,

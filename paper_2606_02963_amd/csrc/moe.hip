@@ -359,7 +359,7 @@ struct GroupedArgs {
   const int32_t* offsets;  // [E + 1]
   const int32_t* tile_off; // [E + 1]
   const float* topk_w;     // [S] routing weights by slot id
-  char* out;               // gate/up: h [S, I] bf16 (expert order); down: y_slot [S, H] bf16 (slot order)
+  char* out;               // gate/up: h [S, I] bf16 (expert order); down: y_slot [S, H] fp32 (slot order)
   int E, k;
   int tiles_n;             // n-tiles of the output
   int tiles_n_grid;        // n-tiles per grid row: tiles_n rounded up to a multiple of 8
@@ -371,10 +371,17 @@ struct GroupedArgs {
   int interleaved;
 };
 
+// LDS of a grouped workgroup: the main loop's two stages, or the output
+// staging of the epilogue — h (bf16, BN/2 columns) for gate/up, and for down
+// the fp32 slot outputs in as few column slabs (F32_PASSES) as fit in the
+// main loop's LDS, so that the fp32 store costs no occupancy.
 template <class TL>
 struct GroupedLds {
   static constexpr int OUT_STAGE = TL::BM * (TL::BN * 2 + 16);
-  static constexpr int BYTES = TL::LOOP_LDS > OUT_STAGE ? TL::LOOP_LDS : OUT_STAGE;
+  static constexpr int f32_stage(int passes) { return TL::BM * (TL::BN / passes * 4 + 16); }
+  static constexpr int F32_PASSES = f32_stage(1) <= TL::LOOP_LDS ? 1 : f32_stage(2) <= TL::LOOP_LDS ? 2 : 4;
+  static constexpr int M1 = TL::LOOP_LDS > OUT_STAGE ? TL::LOOP_LDS : OUT_STAGE;
+  static constexpr int BYTES = M1 > f32_stage(F32_PASSES) ? M1 : f32_stage(F32_PASSES);
 };
 
 // Weight row of tile-local B row ρ. Gate/up tiles interleave 16-row blocks:
@@ -513,7 +520,9 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
     const int64_t ldo = a.ldo;
     const int n0 = tn * TL::BN;
     const int ncols = (int)(a.Nw - n0 < TL::BN ? a.Nw - n0 : TL::BN);
-    store_tile_bf16<TL, TL::BN>(
+    // the weighted slot outputs stay fp32 until the finalize's single
+    // rounding of the token sum
+    store_tile_f32<TL, TL::BN, GroupedLds<TL>::F32_PASSES>(
         lds,
         [&](int fm, int fn, int i, float& v, int& c) {
           v = acc[fm][fn][i];
@@ -522,7 +531,7 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
         },
         [&](int r) -> char* {
           const int row = r0 + r;
-          return row < seg1 ? out + ((int64_t)a.perm[row] * ldo + n0) * 2 : nullptr;
+          return row < seg1 ? out + ((int64_t)a.perm[row] * ldo + n0) * 4 : nullptr;
         },
         ncols);
   }
@@ -534,27 +543,41 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
 // ---------------------------------------------------------------------------
 // finalize: out[t, :] = Σ_j y_slot[t·k + j, :], j ascending, fp32 sum, bf16 out
 // (paper §IV-A, the MoE finalize kernel of Table I). One thread per 8
-// consecutive columns of a token; its K loads are all issued before the
-// first add, so a launch costs one memory round trip whatever K is.
+// consecutive columns of a token; its K slot loads are all issued before the
+// first add, so a launch costs one memory round trip whatever K is. The slot
+// rows are bf16 (the standalone Table I kernel) or fp32 (inside the MoE step,
+// where the down GEMM leaves them unrounded).
 
-template <int K>
-__global__ __launch_bounds__(256) void moe_finalize_kernel(const uint16_t* y_slot, uint16_t* out, int T,
-                                                           int64_t H) {
+template <int K, class Y>
+__global__ __launch_bounds__(256) void moe_finalize_kernel(const Y* y_slot, uint16_t* out, int T, int64_t H) {
   const int64_t cpt = H / 8;
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t t = idx / cpt, c = idx % cpt;
   if (t >= T) return;
-  i32x4 v[K];
-#pragma unroll
-  for (int j = 0; j < K; ++j) v[j] = *reinterpret_cast<const i32x4*>(y_slot + ((t * K + j) * H + c * 8));
   float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  if constexpr (sizeof(Y) == 2) {
+    i32x4 v[K];
 #pragma unroll
-  for (int j = 0; j < K; ++j)
+    for (int j = 0; j < K; ++j) v[j] = *reinterpret_cast<const i32x4*>(y_slot + ((t * K + j) * H + c * 8));
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      acc[2 * q] += bf16_bits_to_f32((uint16_t)(v[j][q] & 0xffff));
-      acc[2 * q + 1] += bf16_bits_to_f32((uint16_t)((uint32_t)v[j][q] >> 16));
-    }
+    for (int j = 0; j < K; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        acc[2 * q] += bf16_bits_to_f32((uint16_t)(v[j][q] & 0xffff));
+        acc[2 * q + 1] += bf16_bits_to_f32((uint16_t)((uint32_t)v[j][q] >> 16));
+      }
+  } else {
+    f32x4 v[K][2];
+#pragma unroll
+    for (int j = 0; j < K; ++j)
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+        v[j][h] = *reinterpret_cast<const f32x4*>(y_slot + ((t * K + j) * H + c * 8 + h * 4));
+#pragma unroll
+    for (int j = 0; j < K; ++j)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) acc[q] += v[j][q >> 2][q & 3];
+  }
   i32x4 o;
 #pragma unroll
   for (int q = 0; q < 4; ++q)
@@ -562,21 +585,22 @@ __global__ __launch_bounds__(256) void moe_finalize_kernel(const uint16_t* y_slo
   *reinterpret_cast<i32x4*>(out + (t * H + c * 8)) = o;
 }
 
-// Enqueue the finalize for top_k = k (1 .. KMAX).
-static void launch_finalize(const void* y_slot, void* out, int64_t T, int64_t H, int k, hipStream_t s) {
+// Enqueue the finalize for top_k = k (1 .. KMAX) over slot rows of type Y.
+template <class Y>
+static hipError_t launch_finalize(const Y* y, void* out, int64_t T, int64_t H, int k, hipStream_t s) {
   const int64_t threads = T * (H / 8);
   const dim3 grid((unsigned)((threads + 255) / 256)), block(256);
-  const uint16_t* y = static_cast<const uint16_t*>(y_slot);
   uint16_t* o = static_cast<uint16_t*>(out);
+  const int t = (int)T;
   switch (k) {
-    case 1: hipLaunchKernelGGL(moe_finalize_kernel<1>, grid, block, 0, s, y, o, (int)T, H); break;
-    case 2: hipLaunchKernelGGL(moe_finalize_kernel<2>, grid, block, 0, s, y, o, (int)T, H); break;
-    case 3: hipLaunchKernelGGL(moe_finalize_kernel<3>, grid, block, 0, s, y, o, (int)T, H); break;
-    case 4: hipLaunchKernelGGL(moe_finalize_kernel<4>, grid, block, 0, s, y, o, (int)T, H); break;
-    case 5: hipLaunchKernelGGL(moe_finalize_kernel<5>, grid, block, 0, s, y, o, (int)T, H); break;
-    case 6: hipLaunchKernelGGL(moe_finalize_kernel<6>, grid, block, 0, s, y, o, (int)T, H); break;
-    case 7: hipLaunchKernelGGL(moe_finalize_kernel<7>, grid, block, 0, s, y, o, (int)T, H); break;
-    default: hipLaunchKernelGGL(moe_finalize_kernel<8>, grid, block, 0, s, y, o, (int)T, H); break;
+    case 1: return launch(moe_finalize_kernel<1, Y>, grid, block, 0, s, y, o, t, H);
+    case 2: return launch(moe_finalize_kernel<2, Y>, grid, block, 0, s, y, o, t, H);
+    case 3: return launch(moe_finalize_kernel<3, Y>, grid, block, 0, s, y, o, t, H);
+    case 4: return launch(moe_finalize_kernel<4, Y>, grid, block, 0, s, y, o, t, H);
+    case 5: return launch(moe_finalize_kernel<5, Y>, grid, block, 0, s, y, o, t, H);
+    case 6: return launch(moe_finalize_kernel<6, Y>, grid, block, 0, s, y, o, t, H);
+    case 7: return launch(moe_finalize_kernel<7, Y>, grid, block, 0, s, y, o, t, H);
+    default: return launch(moe_finalize_kernel<8, Y>, grid, block, 0, s, y, o, t, H);
   }
 }
 static_assert(KMAX == 8, "launch_finalize instantiates top_k 1 .. 8");
@@ -638,7 +662,7 @@ static MoeLayout layout(const moe_desc& d) {
   L.h = o;
   o = align_up(o + (size_t)L.S * (size_t)d.I * 2);
   L.y = o;
-  o = align_up(o + (size_t)L.S * (size_t)d.H * 2);
+  o = align_up(o + (size_t)L.S * (size_t)d.H * 4);
   L.xq = L.sx = L.hq = L.sh = 0;
   if (d.w_dtype == FG_E4M3) {
     L.xq = o;
@@ -701,7 +725,7 @@ static int resident_workgroups() {
 // up interleaved), down tiles BN columns of the output.
 
 template <class TL, int EPI>
-static void launch_grouped(GroupedArgs a, int64_t S, hipStream_t s) {
+static hipError_t launch_grouped(GroupedArgs a, int64_t S, hipStream_t s) {
   a.tiles_n = EPI == EPI_GATEUP ? (int)((a.I + TL::BN / 2 - 1) / (TL::BN / 2)) : (int)((a.Nw + TL::BN - 1) / TL::BN);
   a.tiles_n_grid = (a.tiles_n + 7) / 8 * 8;
   // the m-tile count is known only on the device; its upper bound is
@@ -718,7 +742,7 @@ static void launch_grouped(GroupedArgs a, int64_t S, hipStream_t s) {
     grid = res < upper ? res : upper;
   }
   grid = grid / 8 * 8 > 0 ? grid / 8 * 8 : 8;
-  hipLaunchKernelGGL((grouped_kernel<TL, EPI>), dim3((unsigned)grid), dim3(TL::THREADS), 0, s, a);
+  return launch(grouped_kernel<TL, EPI>, dim3((unsigned)grid), dim3(TL::THREADS), 0, s, a);
 }
 
 }  // namespace fg
@@ -760,12 +784,13 @@ extern "C" fg_status moe_grouped_ffn(const moe_desc* d, const void* tokens, cons
   int32_t* tile_off = reinterpret_cast<int32_t*>(ws + L.tile_off);
   const int64_t S = L.S;
   const int T = (int)d->T;
+  Launches lc;
   if (T == 0) {
     // no tokens: every expert is empty (a fill kernel, not a memset node, so
     // that the call may be captured into a graph)
-    hipLaunchKernelGGL(fill_i32_kernel, dim3((unsigned)((d->E + 1 + 255) / 256)), dim3(256), 0, s, expert_offsets,
-                       d->E + 1, 0);
-    return check_launch(fn);
+    lc.add(launch(fill_i32_kernel, dim3((unsigned)((d->E + 1 + 255) / 256)), dim3(256), 0, s, expert_offsets,
+                  d->E + 1, 0));
+    return check_launch(fn, lc);
   }
   const char* a_tokens = static_cast<const char*>(tokens);
   float* sx = reinterpret_cast<float*>(ws + L.sx);
@@ -774,22 +799,21 @@ extern "C" fg_status moe_grouped_ffn(const moe_desc* d, const void* tokens, cons
   if (f8) {
     a_tokens = ws + L.xq;
     if (L.nblocks > 1)
-      hipLaunchKernelGGL(quantize_rows_kernel, dim3((unsigned)((d->T + 3) / 4)), dim3(256), 0, s, tok16, d->T,
-                         d->H, xq, sx);
+      lc.add(launch(quantize_rows_kernel, dim3((unsigned)((d->T + 3) / 4)), dim3(256), 0, s, tok16, d->T, d->H, xq,
+                    sx));
   }
   int32_t* counts = reinterpret_cast<int32_t*>(ws + L.counts);
   if (L.nblocks == 1) {
     // one routing block; with e4m3 the token quantisation rides in the same launch
     const unsigned qblocks = f8 ? (unsigned)((d->T + 3) / 4) : 0u;
-    hipLaunchKernelGGL(moe_route_kernel<true>, dim3(1 + qblocks), dim3(64 * ROUTE_WAVES), 0, s, router_logits, T,
-                       d->E, d->top_k, topk_idx, topk_w, counts, L.BM, expert_offsets, tile_off, perm, tok16, d->H,
-                       xq, sx);
+    lc.add(launch(moe_route_kernel<true>, dim3(1 + qblocks), dim3(64 * ROUTE_WAVES), 0, s, router_logits, T, d->E,
+                  d->top_k, topk_idx, topk_w, counts, L.BM, expert_offsets, tile_off, perm, tok16, d->H, xq, sx));
   } else {
-    hipLaunchKernelGGL(moe_route_kernel<false>, dim3((unsigned)L.nblocks), dim3(64 * ROUTE_WAVES), 0, s,
-                       router_logits, T, d->E, d->top_k, topk_idx, topk_w, counts, L.BM, expert_offsets, tile_off,
-                       perm, tok16, d->H, xq, sx);
-    hipLaunchKernelGGL(moe_place_kernel, dim3((unsigned)L.nblocks), dim3(64 * PLACE_WAVES), 0, s, topk_idx, counts,
-                       (int)S, d->E, d->top_k, L.nblocks, L.BM, expert_offsets, tile_off, perm);
+    lc.add(launch(moe_route_kernel<false>, dim3((unsigned)L.nblocks), dim3(64 * ROUTE_WAVES), 0, s, router_logits, T,
+                  d->E, d->top_k, topk_idx, topk_w, counts, L.BM, expert_offsets, tile_off, perm, tok16, d->H, xq,
+                  sx));
+    lc.add(launch(moe_place_kernel, dim3((unsigned)L.nblocks), dim3(64 * PLACE_WAVES), 0, s, topk_idx, counts,
+                  (int)S, d->E, d->top_k, L.nblocks, L.BM, expert_offsets, tile_off, perm));
   }
 
   GroupedArgs g;
@@ -813,21 +837,18 @@ extern "C" fg_status moe_grouped_ffn(const moe_desc* d, const void* tokens, cons
   g.K = d->H;
   g.Nw = 2 * d->I;
   g.ldo = d->I;
-  if (f8) {
-    if (use_big_tiles(S, d->E)) launch_grouped<GF8Big, EPI_GATEUP>(g, S, s);
-    else launch_grouped<GF8Small, EPI_GATEUP>(g, S, s);
-  } else {
-    if (use_big_tiles(S, d->E)) launch_grouped<GBf16Big, EPI_GATEUP>(g, S, s);
-    else launch_grouped<GBf16Small, EPI_GATEUP>(g, S, s);
-  }
+  const bool big = use_big_tiles(S, d->E);
+  if (f8)
+    lc.add(big ? launch_grouped<GF8Big, EPI_GATEUP>(g, S, s) : launch_grouped<GF8Small, EPI_GATEUP>(g, S, s));
+  else
+    lc.add(big ? launch_grouped<GBf16Big, EPI_GATEUP>(g, S, s) : launch_grouped<GBf16Small, EPI_GATEUP>(g, S, s));
 
   // down: [S, I] × [H, I]ᵀ → y_slot [S, H] (× routing weight, scattered to slot order)
   const char* hA = ws + L.h;
   float* sh = reinterpret_cast<float*>(ws + L.sh);
   if (f8) {
-    hipLaunchKernelGGL(quantize_rows_kernel, dim3((unsigned)((S + 3) / 4)), dim3(256), 0, s,
-                       reinterpret_cast<const uint16_t*>(ws + L.h), S, d->I,
-                       reinterpret_cast<uint8_t*>(ws + L.hq), sh);
+    lc.add(launch(quantize_rows_kernel, dim3((unsigned)((S + 3) / 4)), dim3(256), 0, s,
+                  reinterpret_cast<const uint16_t*>(ws + L.h), S, d->I, reinterpret_cast<uint8_t*>(ws + L.hq), sh));
     hA = ws + L.hq;
   }
   g.A = hA;
@@ -838,16 +859,13 @@ extern "C" fg_status moe_grouped_ffn(const moe_desc* d, const void* tokens, cons
   g.K = d->I;
   g.Nw = d->H;
   g.ldo = d->H;
-  if (f8) {
-    if (use_big_tiles(S, d->E)) launch_grouped<GF8Big, EPI_DOWN>(g, S, s);
-    else launch_grouped<GF8Small, EPI_DOWN>(g, S, s);
-  } else {
-    if (use_big_tiles(S, d->E)) launch_grouped<GBf16Big, EPI_DOWN>(g, S, s);
-    else launch_grouped<GBf16Small, EPI_DOWN>(g, S, s);
-  }
+  if (f8)
+    lc.add(big ? launch_grouped<GF8Big, EPI_DOWN>(g, S, s) : launch_grouped<GF8Small, EPI_DOWN>(g, S, s));
+  else
+    lc.add(big ? launch_grouped<GBf16Big, EPI_DOWN>(g, S, s) : launch_grouped<GBf16Small, EPI_DOWN>(g, S, s));
 
-  launch_finalize(ws + L.y, out, d->T, d->H, d->top_k, s);
-  return check_launch(fn);
+  lc.add(launch_finalize(reinterpret_cast<const float*>(ws + L.y), out, d->T, d->H, d->top_k, s));
+  return check_launch(fn, lc);
 }
 
 extern "C" fg_status moe_finalize(const void* y_slot, void* out, int64_t T, int64_t H, int32_t top_k, void* stream) {
@@ -860,6 +878,7 @@ extern "C" fg_status moe_finalize(const void* y_slot, void* out, int64_t T, int6
   if (T == 0) return FG_OK;
   if (y_slot == nullptr || out == nullptr) return fail(FG_ERR_INVALID_ARG, "%s: NULL pointer", fn);
   if (!aligned16(y_slot) || !aligned16(out)) return fail(FG_ERR_ALIGNMENT, "%s: pointers must be 16-byte aligned", fn);
-  launch_finalize(y_slot, out, T, H, top_k, static_cast<hipStream_t>(stream));
-  return check_launch(fn);
+  Launches lc;
+  lc.add(launch_finalize(static_cast<const uint16_t*>(y_slot), out, T, H, top_k, static_cast<hipStream_t>(stream)));
+  return check_launch(fn, lc);
 }

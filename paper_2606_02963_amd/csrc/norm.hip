@@ -115,8 +115,9 @@ extern "C" fg_status add_rmsnorm(const void* x, void* residual, const void* weig
     return fail(FG_ERR_INVALID_ARG, "%s: NULL pointer", fn);
   if (!aligned16(x) || !aligned16(residual) || !aligned16(weight) || !aligned16(out))
     return fail(FG_ERR_ALIGNMENT, "%s: pointers must be 16-byte aligned", fn);
-  hipLaunchKernelGGL(add_rmsnorm_kernel, dim3((unsigned)T), dim3(NORM_THREADS), 0, static_cast<hipStream_t>(stream),
-                     static_cast<const uint16_t*>(x), static_cast<uint16_t*>(residual),
-                     static_cast<const uint16_t*>(weight), static_cast<uint16_t*>(out), (int)H, eps);
-  return check_launch(fn);
+  Launches lc;
+  lc.add(launch(add_rmsnorm_kernel, dim3((unsigned)T), dim3(NORM_THREADS), 0, static_cast<hipStream_t>(stream),
+                static_cast<const uint16_t*>(x), static_cast<uint16_t*>(residual),
+                static_cast<const uint16_t*>(weight), static_cast<uint16_t*>(out), (int)H, eps));
+  return check_launch(fn, lc);
 }

@@ -35,7 +35,8 @@ extern "C" fg_status fg_quantize_rows_e4m3(const void* x, int64_t rows, int64_t 
   if (!aligned16(x) || (reinterpret_cast<uintptr_t>(q) & 7u) != 0 || (reinterpret_cast<uintptr_t>(s) & 3u) != 0)
     return fail(FG_ERR_ALIGNMENT, "fg_quantize_rows_e4m3: x must be 16-byte and q 8-byte aligned");
   const unsigned grid = (unsigned)((rows + 3) / 4);
-  hipLaunchKernelGGL(quantize_rows_kernel, dim3(grid), dim3(256), 0, static_cast<hipStream_t>(stream),
-                     static_cast<const uint16_t*>(x), rows, cols, q, s);
-  return check_launch("fg_quantize_rows_e4m3");
+  Launches lc;
+  lc.add(launch(quantize_rows_kernel, dim3(grid), dim3(256), 0, static_cast<hipStream_t>(stream),
+                static_cast<const uint16_t*>(x), rows, cols, q, s));
+  return check_launch("fg_quantize_rows_e4m3", lc);
 }

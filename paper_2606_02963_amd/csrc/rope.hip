@@ -233,7 +233,7 @@ extern "C" fg_status bias_rope_kv_update(const rope_desc* d, const void* qkv, co
   a.log2_base = log2((double)d->rope_base);
   int threads = (a.items + 63) / 64 * 64;
   if (threads > 1024) threads = 1024;
-  hipLaunchKernelGGL(bias_rope_kv_kernel, dim3((unsigned)d->T), dim3(threads), 0, static_cast<hipStream_t>(stream),
-                     a);
-  return check_launch(fn);
+  Launches lc;
+  lc.add(launch(bias_rope_kv_kernel, dim3((unsigned)d->T), dim3(threads), 0, static_cast<hipStream_t>(stream), a));
+  return check_launch(fn, lc);
 }

@@ -316,3 +316,16 @@ def test_header_is_plain_c():
         r = subprocess.run([gcc, std, "-Wall", "-Wextra", "-pedantic", "-Werror", "-fsyntax-only", "-x", lang,
                             HEADER], capture_output=True, text=True)
         assert r.returncode == 0, r.stderr
+
+
+def test_trace_validation_without_gpu():
+    """The launch-trace calls reject bad requests before any HIP call."""
+    for cap in (0, -3, (1 << 20) + 1):
+        with pytest.raises(L.FgError) as ei:
+            L.fg_trace_begin(cap)
+        assert ei.value.status == L.FG_ERR_INVALID_ARG
+    assert L.fg_trace_end() == 0                         # closing with nothing traced
+    for i in (0, -1, 5):
+        with pytest.raises(L.FgError) as ei:
+            L.fg_trace_read(i)
+        assert ei.value.status == L.FG_ERR_INVALID_ARG

@@ -6,8 +6,10 @@ under the RMS-floored relative error, ≤ 1e-2 for bf16 weights and ≤ 4e-2 for
 the e4m3 (W8A8) variant. Small shapes cover ragged experts, both row-tile
 sizes, empty experts, ties in the logits, the gate/up clamps, the
 interleaved gate/up layout and E = 1; the full gpt-oss-20b-like geometry
-(H = I = 2880, E = 32, top-4) is run at T = 64 (all tokens checked) and
-T = 4096 (sampled tokens; routing checked in full)."""
+(H = I = 2880, E = 32, top-4) is run at T = 64 and T = 4096, every token
+checked. The oracle's output is the unrounded routing-weighted sum of the
+slot outputs; the tolerance covers the kernel's bf16 output rounding and its
+fp32 arithmetic."""
 
 import numpy as np
 import pytest
@@ -137,9 +139,8 @@ def test_moe_full_geometry_decode(name):
 
 
 @pytest.mark.parametrize("name", ["moe_prefill_bf16", "moe_prefill_e4m3"])
-def test_moe_full_geometry_prefill_sampled(name):
-    spec = MOE_SPECS[name]
-    run_moe(spec, tokens=[0, 1, 2, 777, 2048, 3001, 4094, 4095])
+def test_moe_full_geometry_prefill(name):
+    run_moe(MOE_SPECS[name])
 
 
 def test_quantize_rows_e4m3_bit_exact():
