@@ -1,59 +1,85 @@
 #!/usr/bin/env python3
-"""Benchmark: fused bf16 GEMM + GELU-tanh/clamp tail on one MI355X.
+"""Benchmark of the fused GEMM + tail library on one MI355X.
 
-Workload (the configuration the headline metric is quoted on):
-x[1024, 8192] ~ N(0,1), W[8192, 8192] and b[8192] ~ U(±1/√8192), bf16 inputs,
-y = clamp(GELU_tanh((x·Wᵀ + b)·0.5), −1, 1), bf16 output, fp32 accumulation.
-One step = one fused launch over that batch, inputs resident in HBM.
+Default workload (the largest single-GPU configuration): one MoE expert-FFN
+step of a gpt-oss-20b-like layer, T = 4096 tokens, hidden 2880, 32 experts,
+top-4, bf16 weights ~ N(0, 0.02), clamped SwiGLU: routing, permutation, the
+grouped gate/up GEMM with the SwiGLU epilogue, the grouped down GEMM with the
+routing weight, and the finalize, all on the device with inputs resident in
+HBM. Other workloads: the dense fused GEMM + tail configurations, the e4m3
+MoE variants, the decode step, and the Table I kernels.
 
-Prints ONE JSON line with the fused kernel's TFLOP/s (``value``), its
-roofline fraction against the dense bf16 MFMA peak, the unfused sequence
-(vendor GEMM + one eager kernel per tail op) and the GEMM alone timed beside
-it, and the fp64 CPU oracle timed on a bounded sample of rows.
+Timing: W untimed warmup steps (after about a second of untimed work so
+that clocks settle), then seven repeats, each timing a multiple of K steps
+with HIP events on the stream the library launches on, bracketed by device
+synchronisation, and lasting at least --min-repeat-seconds; ``value`` and
+``ms_per_step`` are the median over the repeats (their coefficient of
+variation is reported beside it). The shader and memory clocks are sampled
+from sysfs during the repeats. A separate pass of K steps traces every
+launch with HIP events (fg_trace_begin) to give each kernel's average
+duration; ``roofline`` is that of the dominant kernel, ``step_roofline`` that
+of the whole step. The unfused PyTorch sequence is timed the same way, and
+the fp64 CPU oracle on a bounded sample whose outputs are also compared.
+
+Prints ONE JSON line.
 
 Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu-baseline]
-                       [--workload gelu_clamp|gelu_clamp_e4m3|lse|silu_gn|tiny_f32|scale_lse_mish|gn_swish_mul_swish|
-                                   gn_lrelu_sum|swish_sum_gn|moe_{prefill,decode}_{bf16,e4m3}|
+                       [--workload moe_prefill_bf16|moe_prefill_e4m3|moe_decode_bf16|moe_decode_e4m3|
+                                   gelu_clamp|gelu_clamp_e4m3|lse|silu_gn|tiny_f32|scale_lse_mish|
+                                   gn_swish_mul_swish|gn_lrelu_sum|swish_sum_gn|
                                    moe_finalize|add_rmsnorm|rope_kv]
 """
 
 import argparse
+import glob
 import hashlib
 import json
+import math
 import os
+import re
+import statistics
+import subprocess
 import sys
+import threading
 import time
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
-PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA, published
-PEAK_FP8_TFLOPS = 5000.0       # MI355X dense fp8 MFMA, published
+# MI355X published dense peaks (no sparsity)
+PEAK_BF16_TFLOPS = 2516.6
+PEAK_FP8_TFLOPS = 5033.2
+PEAK_FP32_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
+PEAK_SCLK_MHZ = 2400.0
 PROFILES = os.path.join(ROOT, "profiles")
 KERNEL_SOURCES = ["fg_tile.hpp", "fg_epilogue.hpp", "fgemm.hip"]
 MOE_KERNEL_SOURCES = ["fg_tile.hpp", "fg_quant.hpp", "moe.hip", "quant.hip"]
+REPEATS = 7
 
 
 def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=50)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--warmup-seconds", type=float, default=1.0,
                     help="extra untimed work first, so clocks settle before timing")
+    ap.add_argument("--min-repeat-seconds", type=float, default=1.0,
+                    help="each of the seven timed repeats runs whole multiples of --steps steps for at "
+                         "least this long")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-unfused", action="store_true")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="target oracle sample time")
     ap.add_argument("--copy-calibration-mb", type=int, default=0,
                     help="after the measurement, run a plain device-to-device copy of this many MiB "
                          "(3 times); its HBM counters calibrate rocprofv3 FETCH_SIZE/WRITE_SIZE")
-    ap.add_argument("--workload", default="gelu_clamp",
-                    choices=["gelu_clamp", "gelu_clamp_e4m3", "lse", "silu_gn", "tiny_f32", "scale_lse_mish",
-                             "gn_swish_mul_swish", "gn_lrelu_sum", "swish_sum_gn", "moe_prefill_bf16",
-                             "moe_prefill_e4m3", "moe_decode_bf16", "moe_decode_e4m3", "moe_finalize", "add_rmsnorm",
-                             "rope_kv"],
-                    help="gelu_clamp (default) is the headline workload; the others are the "
+    ap.add_argument("--workload", default="moe_prefill_bf16",
+                    choices=["moe_prefill_bf16", "moe_prefill_e4m3", "moe_decode_bf16", "moe_decode_e4m3",
+                             "gelu_clamp", "gelu_clamp_e4m3", "lse", "silu_gn", "tiny_f32", "scale_lse_mish",
+                             "gn_swish_mul_swish", "gn_lrelu_sum", "swish_sum_gn", "moe_finalize",
+                             "add_rmsnorm", "rope_kv"],
+                    help="moe_prefill_bf16 (default) is the headline workload; the others are the "
                          "remaining configurations, measured the same way")
     return ap.parse_args()
 
@@ -96,28 +122,142 @@ def settle(fn, seconds, torch):
         torch.cuda.synchronize()
 
 
-def time_steps(fn, steps, warmup, torch):
-    for _ in range(warmup):
-        fn()
+def time_block(fn, n, torch):
+    """Milliseconds for n back-to-back steps: HIP events on the current
+    stream (where the library launches), device synchronised before and
+    after."""
     torch.cuda.synchronize()
     start, stop = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     start.record()
-    for _ in range(steps):
+    for _ in range(n):
         fn()
     stop.record()
     torch.cuda.synchronize()
-    return start.elapsed_time(stop) / steps      # ms per step
+    return start.elapsed_time(stop)
 
 
-def repeat_stats(fn, steps, torch, count=7):
-    """Seven further timings of `steps` steps each, after the reported one:
-    the median step time and the coefficient of variation across them (the
-    run-to-run spread on one box; the reported value is the first timing)."""
-    import statistics
-    ms = [time_steps(fn, steps, 0, torch) for _ in range(count)]
-    med = statistics.median(ms)
-    cv = statistics.pstdev(ms) / statistics.fmean(ms)
-    return {"count": count, "ms_per_step_median": round(med, 5), "cv": round(cv, 5)}
+def timed_repeats(fn, steps, warmup, min_seconds, torch, repeats=REPEATS):
+    """`warmup` untimed steps, then `repeats` timings, each of blocks × steps
+    back-to-back steps where blocks is the smallest count that makes one
+    repeat last at least `min_seconds`. Returns the median ms per step and
+    the spread."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    probe = time_block(fn, steps, torch)
+    blocks = max(1, math.ceil(min_seconds * 1e3 / max(probe, 1e-6)))
+    per = [time_block(fn, steps * blocks, torch) / (steps * blocks) for _ in range(repeats)]
+    med = statistics.median(per)
+    return {"ms_per_step": med, "repeats": repeats, "steps_per_repeat": steps * blocks,
+            "seconds_per_repeat": round(med * steps * blocks / 1e3, 3),
+            "ms_per_step_each": [round(v, 5) for v in per],
+            "cv": round(statistics.pstdev(per) / statistics.fmean(per), 5)}
+
+
+class ClockSampler:
+    """Samples the GPU's current shader (sclk) and memory (mclk) clock from
+    sysfs (pp_dpm_sclk / pp_dpm_mclk, the level marked '*') every 50 ms
+    while active. The device is found by the PCI address torch reports for
+    device 0; with no readable file the summary says so."""
+
+    def __init__(self, torch):
+        self.paths = {}
+        try:
+            p = torch.cuda.get_device_properties(0)
+            addr = f"{p.pci_domain_id:04x}:{p.pci_bus_id:02x}:{p.pci_device_id:02x}"
+            cands = sorted(glob.glob(f"/sys/bus/pci/devices/{addr}.*"))
+        except Exception:
+            cands = []
+        if not cands:
+            cards = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+            cands = [os.path.dirname(cards[0])] if len(cards) == 1 else []
+        for d in cands:
+            for clk in ("sclk", "mclk"):
+                f = os.path.join(d, f"pp_dpm_{clk}")
+                if os.access(f, os.R_OK):
+                    self.paths[clk] = f
+            if self.paths:
+                break
+        self.samples = {k: [] for k in self.paths}
+        self._stop = threading.Event()
+        self._thread = None
+
+    @staticmethod
+    def _read(path):
+        try:
+            with open(path) as fh:
+                for line in fh:
+                    if "*" in line:
+                        m = re.search(r"(\d+)\s*[Mm][Hh]z", line)
+                        return int(m.group(1)) if m else None
+        except OSError:
+            return None
+        return None
+
+    def _run(self):
+        while not self._stop.is_set():
+            for k, f in self.paths.items():
+                v = self._read(f)
+                if v is not None:
+                    self.samples[k].append(v)
+            self._stop.wait(0.05)
+
+    def __enter__(self):
+        if self.paths:
+            self._thread = threading.Thread(target=self._run, daemon=True)
+            self._thread.start()
+        return self
+
+    def __exit__(self, *exc):
+        self._stop.set()
+        if self._thread is not None:
+            self._thread.join()
+
+    def summary(self):
+        out = {"source": self.paths.get("sclk", "unavailable (no readable pp_dpm_sclk)")}
+        for k, v in self.samples.items():
+            if v:
+                out[f"{k}_mhz"] = {"median": statistics.median(v), "min": min(v), "max": max(v),
+                                   "samples": len(v)}
+        return out
+
+
+def demangle(names):
+    try:
+        r = subprocess.run(["c++filt"], input="\n".join(names), capture_output=True, text=True, timeout=10)
+        out = r.stdout.splitlines()
+        if r.returncode == 0 and len(out) == len(names):
+            return out
+    except (OSError, subprocess.SubprocessError):
+        pass
+    return list(names)
+
+
+def trace_kernels(fn, steps, torch):
+    """Run `steps` steps with the library's launch trace open and return,
+    per kernel, the number of launches and the average and total time
+    between the HIP events recorded around each launch."""
+    from paper_2606_02963_amd import _lib
+    torch.cuda.synchronize()
+    _lib.fg_trace_begin(steps * 64)
+    try:
+        for _ in range(steps):
+            fn()
+    finally:
+        n = _lib.fg_trace_end()
+    torch.cuda.synchronize()
+    rows = [_lib.fg_trace_read(i) for i in range(n)]
+    names = demangle(sorted({name for _, name in rows}))
+    pretty = dict(zip(sorted({name for _, name in rows}), names))
+    per = {}
+    for ms, name in rows:
+        per.setdefault(pretty[name], []).append(ms)
+    return {k: {"launches": len(v), "avg_us": round(1e3 * statistics.fmean(v), 2),
+                "total_ms": round(sum(v), 4)} for k, v in per.items()}
+
+
+def dominant(kernels):
+    return max(kernels.items(), key=lambda kv: kv[1]["total_ms"])
 
 
 FGEMM_WORKLOADS = {"gelu_clamp": "bf16_gelu_clamp", "lse": "bf16_lse", "silu_gn": "bf16_silu_gn",
@@ -134,14 +274,34 @@ TAIL_TEXT = {"bf16_gelu_clamp": "(x0.5, GELU_tanh, clamp[-1,1])", "bf16_lse": "(
              "e4m3_gelu_clamp": "(per-row scales, x0.5, GELU_tanh, clamp[-1,1])"}
 
 
-def base_result(args, metric_value, ms, dtype, data, config, roofline):
+def base_result(args, metric_value, tim, dtype, data, config, roofline):
     return {
         "metric": "fused GEMM+epilogue TFLOP/s (% of MI355X MFMA peak) vs unfused sequence",
         "value": round(metric_value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True,
+        "warmup": args.warmup, "ms_per_step": round(tim["ms_per_step"], 5), "higher_is_better": True,
         "scaling": "weak", "vs_baseline": None, "dtype": dtype, "data": data, "config": config,
         "roofline": roofline,
     }
+
+
+def timing_record(tim, clk):
+    t = dict(tim)
+    t["ms_per_step"] = round(t["ms_per_step"], 5)
+    t["clocks"] = clk.summary()
+    sclk = t["clocks"].get("sclk_mhz", {}).get("median")
+    if sclk:
+        t["peak_scale_at_sampled_sclk"] = round(sclk / PEAK_SCLK_MHZ, 4)
+    return t
+
+
+def measure(fn, args, torch):
+    """Settle, then the seven timed repeats with the clocks sampled, then the
+    traced pass. Returns (timing, clock sampler, per-kernel trace)."""
+    settle(fn, args.warmup_seconds, torch)
+    with ClockSampler(torch) as clk:
+        tim = timed_repeats(fn, args.steps, args.warmup, args.min_repeat_seconds, torch)
+    kernels = trace_kernels(fn, args.steps, torch)
+    return tim, clk, kernels
 
 
 def bench_fgemm(args, torch, np):
@@ -176,28 +336,30 @@ def bench_fgemm(args, torch, np):
                             out_dtype=spec.out, out=out, workspace=ws, post_ops=spec.post_ops,
                             x_scale=sx, w_scale=sw)
 
-    settle(fused, args.warmup_seconds, torch)
-    ms = time_steps(fused, args.steps, args.warmup, torch)
-    reps = repeat_stats(fused, args.steps, torch)
+    tim, clk, kernels = measure(fused, args, torch)
+    ms = tim["ms_per_step"]
     flops = spec.flops()
     tflops = flops / (ms * 1e-3) / 1e12
-    peak = {"bf16": PEAK_BF16_TFLOPS, "e4m3": PEAK_FP8_TFLOPS, "f32": 157.3}[spec.dtype]
-    # the GEMM launch dominates; with a row LogSumExp the step also holds the
-    # small combine launch, so the step time bounds the GEMM launch from above
-    achieved = tflops
+    peak = {"bf16": PEAK_BF16_TFLOPS, "e4m3": PEAK_FP8_TFLOPS, "f32": PEAK_FP32_TFLOPS}[spec.dtype]
+    kname, kst = dominant(kernels)
+    k_tflops = flops / (kst["avg_us"] * 1e-6) / 1e12
     name = f"fgemm_{spec.name}_{spec.M}x{spec.N}x{spec.K}"
     result = base_result(
-        args, tflops, ms, spec.dtype,
+        args, tflops, tim, spec.dtype,
         "synthetic (seeded: x ~ N(0,1), W, b ~ U(+-a); see paper_2606_02963_amd/synth.py)",
         {"workload": f"{spec.dtype} GEMM + {TAIL_TEXT[spec.name]} tail, x[{spec.M},{spec.K}] "
                      f"W[{spec.N},{spec.K}] -> {spec.out}"
                      f"[{spec.M}{'' if spec.reduction == 'lse' else ',' + str(spec.N)}]",
          "M": spec.M, "N": spec.N, "K": spec.K, "tile": f"{info['tile_m']}x{info['tile_n']}",
          "workgroups": info["workgroups"], "launches_per_step": info["launches"]},
-        {"bound": "mfma", "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s",
-         "frac": round(achieved / peak, 4), "traffic": measured_traffic(name),
-         "algorithmic_flops_per_launch": flops, "algorithmic_bytes_per_launch": spec.bytes()})
-    result["repeats"] = reps
+        {"bound": "mfma", "kernel": kname, "achieved": round(k_tflops, 2), "peak": peak, "unit": "TFLOP/s",
+         "frac": round(k_tflops / peak, 4), "traffic": measured_traffic(name),
+         "avg_launch_us": kst["avg_us"], "algorithmic_flops_per_launch": flops,
+         "algorithmic_bytes_per_launch": spec.bytes()})
+    result["step_roofline"] = {"bound": "mfma", "achieved": round(tflops, 2), "peak": peak, "unit": "TFLOP/s",
+                               "frac": round(tflops / peak, 4), "scope": "whole step (all launches)"}
+    result["timing"] = timing_record(tim, clk)
+    result["kernels"] = kernels
 
     if not args.no_unfused:
         tdt = torch.float32 if spec.dtype == "f32" else torch.bfloat16
@@ -245,28 +407,33 @@ def bench_fgemm(args, torch, np):
             return eager_ops(z, spec.post_ops)
 
         try:
-            ms_u = time_steps(unfused, args.steps, args.warmup, torch)
-            ms_g = time_steps(vendor_mm, args.steps, args.warmup, torch)
+            tu = timed_repeats(unfused, args.steps, args.warmup, args.min_repeat_seconds, torch)
+            tg = timed_repeats(vendor_mm, args.steps, args.warmup, args.min_repeat_seconds, torch)
         except RuntimeError as e:         # a torch build without row-wise fp8 scaling
             result["unfused"] = {"ms": None, "error": str(e).splitlines()[0][:200]}
         else:
-            result["unfused"] = {"ms": round(ms_u, 5), "tflops": round(flops / (ms_u * 1e-3) / 1e12, 2),
+            ms_u, ms_g = tu["ms_per_step"], tg["ms_per_step"]
+            result["unfused"] = {"ms": round(ms_u, 5), "cv": tu["cv"],
+                                 "tflops": round(flops / (ms_u * 1e-3) / 1e12, 2),
                                  "sequence": ("torch._scaled_mm (vendor fp8 GEMM, row-wise scales)"
                                               if spec.dtype == "e4m3" else "torch.mm (vendor BLAS)")
                                  + " then one eager kernel per tail op"}
-            result["gemm_only"] = {"ms": round(ms_g, 5), "tflops": round(flops / (ms_g * 1e-3) / 1e12, 2)}
+            result["gemm_only"] = {"ms": round(ms_g, 5), "cv": tg["cv"],
+                                   "tflops": round(flops / (ms_g * 1e-3) / 1e12, 2)}
             result["speedup_vs_unfused"] = round(ms_u / ms, 3)
 
     if not args.no_cpu_baseline:
         torch.cuda.synchronize()
         cpu = cpu_oracle_fgemm(spec, inp, args.cpu_seconds, out, np)
         result["cpu_baseline"], rep = cpu
-        result["parity_sample"] = {"rel_err": rep.rel_err, "tol": rep.tol, "ok": bool(rep.ok)}
+        result["parity_sample"] = {"rel_err": rep.rel_err, "tol": rep.tol, "ok": bool(rep.ok),
+                                   "rows_compared": int(cpu[0]["rows"])}
     return result
 
 
 def cpu_oracle_fgemm(spec, inp, budget_s, out, np):
-    """Time the fp64 oracle on a growing sample of rows until ~budget_s."""
+    """Time the fp64 oracle on a growing sample of rows until ~budget_s (or
+    all rows), and compare every row it computed with the GPU output."""
     from threadpoolctl import threadpool_info
     from oracle import bf16_decode, compare, e4m3_decode, ref_fgemm
 
@@ -278,7 +445,7 @@ def cpu_oracle_fgemm(spec, inp, budget_s, out, np):
         x64, W64 = dec(inp["x"]), dec(inp["W"])
     b = inp["b"].astype(np.float64)
     got = out.float().cpu().numpy().astype(np.float64)
-    rows, t_total, flops_total, n_rows, first = 8, 0.0, 0.0, 0, None
+    rows, t_total, flops_total, n_rows, refs = 8, 0.0, 0.0, 0, []
     while t_total < budget_s and n_rows < spec.M:
         r = min(rows, spec.M - n_rows)
         sel = slice(n_rows, n_rows + r)
@@ -286,18 +453,43 @@ def cpu_oracle_fgemm(spec, inp, budget_s, out, np):
         ref = ref_fgemm(x64[sel], W64, b, spec.ops, spec.reduction, spec.gn_groups, spec.gn_eps,
                         inp.get("gamma"), inp.get("beta"), spec.post_ops)
         t_total += time.perf_counter() - t0
-        if first is None:
-            first = (sel, ref)
+        refs.append(ref)
         flops_total += 2.0 * r * spec.N * spec.K
         n_rows += r
         rows *= 2
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
-    rep = compare(got[first[0]], first[1], {"f32": "f32", "bf16": "bf16", "e4m3": "e4m3"}[spec.dtype])
+    rep = compare(got[:n_rows], np.concatenate(refs), {"f32": "f32", "bf16": "bf16", "e4m3": "e4m3"}[spec.dtype])
     return ({"value": flops_total / t_total / 1e12, "unit": "TFLOP/s", "cores": int(threads),
              "kind": "oracle",
              "sample": f"{n_rows} of {spec.M} output rows (all {spec.N} columns, K={spec.K}), "
                        f"fp64 numpy matmul + tail, {t_total:.1f} s",
-             "seconds": round(t_total, 2)}, rep)
+             "seconds": round(t_total, 2), "rows": n_rows}, rep)
+
+
+def grouped_epi(kernel_name):
+    """0 for the gate/up grouped GEMM, 1 for the down GEMM, None otherwise."""
+    m = re.search(r"grouped_kernel<.*,\s*([01])>\(", kernel_name) or \
+        re.search(r"grouped_kernel.*Li([01])EEEvNS_11GroupedArgsE", kernel_name)
+    return int(m.group(1)) if m else None
+
+
+def moe_kernel_work(spec, epi, active, S):
+    """Algorithmic FLOP and bytes of one launch of a grouped GEMM: the
+    weights of the experts that receive a slot read once, the activation
+    rows read once, the output written once."""
+    es = 1 if spec.w_dtype == "e4m3" else 2
+    H, I = spec.H, spec.I
+    if epi == 0:
+        flops = 2.0 * S * H * 2 * I
+        nbytes = active * 2 * I * H * es + spec.T * H * es + S * I * 2
+        if es == 1:
+            nbytes += active * 2 * I * 4 + spec.T * 4
+    else:
+        flops = 2.0 * S * I * H
+        nbytes = active * H * I * es + S * I * es + S * H * 4
+        if es == 1:
+            nbytes += active * H * 4 + S * 4
+    return flops, nbytes
 
 
 def bench_moe(args, torch, np):
@@ -315,43 +507,61 @@ def bench_moe(args, torch, np):
     else:
         wgu, wd = torch.from_numpy(w["w_gate_up"]).to(dev), torch.from_numpy(w["w_down"]).to(dev)
         sgu, sd = torch.from_numpy(w["s_gate_up"]).to(dev), torch.from_numpy(w["s_down"]).to(dev)
-    del w
     bufs = api.moe_ffn(x, lg, wgu, wd, sgu, sd, top_k=spec.k)
 
     def fused():
         api.moe_ffn(x, lg, wgu, wd, sgu, sd, top_k=spec.k, buffers=bufs)
 
-    settle(fused, args.warmup_seconds, torch)
-    ms = time_steps(fused, args.steps, args.warmup, torch)
-    reps = repeat_stats(fused, args.steps, torch)
+    tim, clk, kernels = measure(fused, args, torch)
+    ms = tim["ms_per_step"]
     counts = np.diff(bufs.offsets.cpu().numpy())
     active = int(np.sum(counts > 0))
+    S = spec.T * spec.k
     flops = spec.flops()
     nbytes = spec.bytes(active)
     tflops = flops / (ms * 1e-3) / 1e12
     gbs = nbytes / (ms * 1e-3) / 1e9
     decode = spec.T <= 256
-    peak_c = PEAK_BF16_TFLOPS if spec.w_dtype == "bf16" else 5000.0
-    roof = ({"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-             "frac": round(gbs / PEAK_HBM_GBS, 4)} if decode else
-            {"bound": "mfma", "achieved": round(tflops, 2), "peak": peak_c, "unit": "TFLOP/s",
-             "frac": round(tflops / peak_c, 4)})
-    roof.update({"traffic": measured_traffic(spec.name, MOE_KERNEL_SOURCES),
-                 "scope": "whole step (all launches)",
-                 "algorithmic_flops": flops, "algorithmic_bytes": nbytes, "active_experts": active})
+    peak_c = PEAK_BF16_TFLOPS if spec.w_dtype == "bf16" else PEAK_FP8_TFLOPS
+    kname, kst = dominant(kernels)
+    epi = grouped_epi(kname)
+    if epi is None:
+        raise RuntimeError(f"the dominant kernel of the MoE step is not a grouped GEMM: {kname}")
+    k_flops, k_bytes = moe_kernel_work(spec, epi, active, S)
+    sec = kst["avg_us"] * 1e-6
+    common = {"kernel": kname, "avg_launch_us": kst["avg_us"], "algorithmic_flops_per_launch": k_flops,
+              "algorithmic_bytes_per_launch": k_bytes,
+              "traffic": measured_traffic(f"{spec.name}_{'gateup' if epi == 0 else 'down'}", MOE_KERNEL_SOURCES)}
+    if decode:
+        roof = {"bound": "hbm", "achieved": round(k_bytes / sec / 1e9, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(k_bytes / sec / 1e9 / PEAK_HBM_GBS, 4), **common}
+        step_roof = {"bound": "hbm", "achieved": round(gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": round(gbs / PEAK_HBM_GBS, 4)}
+    else:
+        roof = {"bound": "mfma", "achieved": round(k_flops / sec / 1e12, 2), "peak": peak_c, "unit": "TFLOP/s",
+                "frac": round(k_flops / sec / 1e12 / peak_c, 4), **common}
+        step_roof = {"bound": "mfma", "achieved": round(tflops, 2), "peak": peak_c, "unit": "TFLOP/s",
+                     "frac": round(tflops / peak_c, 4)}
+    step_roof.update({"scope": "whole step (all launches)", "algorithmic_flops": flops,
+                      "algorithmic_bytes": nbytes, "active_experts": active,
+                      "traffic": measured_traffic(spec.name, MOE_KERNEL_SOURCES)})
     result = base_result(
-        args, tflops, ms, "e4m3" if spec.w_dtype == "e4m3" else "bf16",
+        args, tflops, tim, "e4m3" if spec.w_dtype == "e4m3" else "bf16",
         "synthetic (seeded: logits, x ~ N(0,1); W ~ N(0,0.02); see paper_2606_02963_amd/synth.py)",
         {"workload": f"MoE expert FFN step T={spec.T} H={spec.H} I={spec.I} E={spec.E} top-{spec.k} "
                      f"{spec.w_dtype} weights, clamped SwiGLU",
          "T": spec.T, "H": spec.H, "I": spec.I, "E": spec.E, "top_k": spec.k}, roof)
+    result["step_roofline"] = step_roof
     result["hbm_gbs"] = round(gbs, 1)
-    result["repeats"] = reps
+    result["timing"] = timing_record(tim, clk)
+    result["kernels"] = kernels
     if not args.no_cpu_baseline:
         torch.cuda.synchronize()
-        cpu, rep = cpu_oracle_moe(spec, act, bufs.out, nbytes, decode, np, torch)
+        cpu, rep = cpu_oracle_moe(spec, act, w, bufs.out, nbytes, decode, np, torch)
         result["cpu_baseline"] = cpu
-        result["parity_sample"] = {"rel_err": rep.rel_err, "tol": rep.tol, "ok": bool(rep.ok)}
+        result["parity_sample"] = {"rel_err": rep.rel_err, "tol": rep.tol, "ok": bool(rep.ok),
+                                   "tokens_compared": cpu["tokens"]}
+    del w
 
     if not args.no_unfused:
         # The eager PyTorch sequence: top-k and softmax, a stable argsort of the
@@ -402,11 +612,13 @@ def bench_moe(args, torch, np):
             return ys.view(-1, k, spec.H).float().sum(1).to(torch.bfloat16)
 
         try:
-            ms_u = time_steps(unfused, args.steps, args.warmup, torch)
+            tu = timed_repeats(unfused, args.steps, args.warmup, args.min_repeat_seconds, torch)
         except RuntimeError as e:         # a torch build without row-wise fp8 scaling
             result["unfused"] = {"ms": None, "error": str(e).splitlines()[0][:200]}
         else:
-            result["unfused"] = {"ms": round(ms_u, 5), "tflops": round(flops / (ms_u * 1e-3) / 1e12, 2),
+            ms_u = tu["ms_per_step"]
+            result["unfused"] = {"ms": round(ms_u, 5), "cv": tu["cv"],
+                                 "tflops": round(flops / (ms_u * 1e-3) / 1e12, 2),
                                  "hbm_gbs": round(nbytes / (ms_u * 1e-3) / 1e9, 1),
                                  "sequence": "eager torch: topk, softmax, stable argsort, per-expert "
                                              + ("row quantisation + torch._scaled_mm (fp8) + elementwise "
@@ -417,15 +629,14 @@ def bench_moe(args, torch, np):
     return result
 
 
-def cpu_oracle_moe(spec, act, out, step_bytes, decode, np, torch):
+def cpu_oracle_moe(spec, act, w, out, step_bytes, decode, np, torch):
     """Time the fp64 oracle's MoE step on the host: the whole step at decode
-    size (T = 64), the first 64 tokens of the prefill batch otherwise. The
-    oracle decodes each expert's weights to fp64 as part of its work."""
+    size (T = 64), the first 64 tokens of the prefill batch otherwise, and
+    compare every token it computed with the GPU output. The oracle decodes
+    each expert's weights to fp64 as part of its work."""
     from threadpoolctl import threadpool_info
     from oracle import bf16_decode, compare, e4m3_decode, ref_moe
-    from paper_2606_02963_amd.synth import make_moe_weights
 
-    w = make_moe_weights(spec, 0)
     if spec.w_dtype == "bf16":
         weights = lambda e: (bf16_decode(w["w_gate_up"][e]), bf16_decode(w["w_down"][e]))  # noqa: E731
     else:
@@ -452,7 +663,7 @@ def cpu_oracle_moe(spec, act, out, step_bytes, decode, np, torch):
              "sample": (f"the whole T={spec.T} step" if tokens is None else
                         f"{n} of {spec.T} tokens (their {n * spec.k} slots through all experts)") +
                        f", fp64 numpy incl. decoding the expert weights, {sec:.1f} s",
-             "seconds": round(sec, 2)}, rep)
+             "seconds": round(sec, 2), "tokens": int(n)}, rep)
 
 
 def bench_finalize(args, torch, np):
@@ -482,7 +693,7 @@ def bench_finalize(args, torch, np):
         if not torch.equal(out, eager):
             raise RuntimeError("graph replay of moe_finalize differs from the eager launch")
         settle(g.replay, min(args.warmup_seconds, 0.3), torch)
-        ms = time_steps(g.replay, max(args.steps // 5, 5), max(args.warmup // 5, 2), torch) / reps
+        ms = timed_repeats(g.replay, max(args.steps // 5, 2), max(args.warmup // 5, 2), min(args.min_repeat_seconds, 0.25), torch)["ms_per_step"] / reps
         nbytes = (T * k * H + T * H) * 2
         sweep[T] = {"us": round(ms * 1e3, 3), "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1), "bytes": nbytes}
     T = FINALIZE_BATCHES[-1]
@@ -539,7 +750,7 @@ def bench_add_rmsnorm(args, torch, np):
             for _ in range(reps):
                 api.add_rmsnorm(x, r, w, out=out)
         settle(g.replay, min(args.warmup_seconds, 0.3), torch)
-        ms = time_steps(g.replay, max(args.steps // 5, 5), max(args.warmup // 5, 2), torch) / reps
+        ms = timed_repeats(g.replay, max(args.steps // 5, 2), max(args.warmup // 5, 2), min(args.min_repeat_seconds, 0.25), torch)["ms_per_step"] / reps
         nbytes = 4 * T * H * 2 + H * 2
         sweep[T] = {"us": round(ms * 1e3, 3), "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1), "bytes": nbytes}
     T = FINALIZE_BATCHES[-1]
@@ -609,7 +820,7 @@ def bench_rope_kv(args, torch, np):
         if not (torch.equal(q, eager_q) and torch.equal(cache, eager_c)):
             raise RuntimeError("graph replay of bias_rope_kv_update differs from the eager launch")
         settle(g.replay, min(args.warmup_seconds, 0.3), torch)
-        ms = time_steps(g.replay, max(args.steps // 5, 5), max(args.warmup // 5, 2), torch) / reps
+        ms = timed_repeats(g.replay, max(args.steps // 5, 2), max(args.warmup // 5, 2), min(args.min_repeat_seconds, 0.25), torch)["ms_per_step"] / reps
         nbytes = spec.bytes()
         sweep[T] = {"us": round(ms * 1e3, 3), "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1), "bytes": nbytes}
     T = FINALIZE_BATCHES[-1]
