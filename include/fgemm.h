@@ -226,6 +226,33 @@ fg_status moe_grouped_ffn(const moe_desc *d, const void *tokens,
                           void *workspace, size_t ws_bytes, void *stream);
 
 /*
+ * moe_grouped_ffn_noalloc — moe_grouped_ffn for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving loops
+ * and harnesses that forbid allocation. Same arguments, semantics and
+ * results as moe_grouped_ffn, without workspace arguments: the workspace is
+ * a static device array of moe_noalloc_scratch_bytes() bytes (64 MiB) inside
+ * the library, one per GPU the library runs on, held until the process ends.
+ * The call itself allocates nothing (the array's address is looked up once
+ * per device on the first call there). Problems whose
+ * moe_workspace_bytes(d) exceeds the array are rejected with
+ * FG_ERR_UNSUPPORTED (at H = I = 2880, E = 32, top-4: up to about 970
+ * tokens with bf16 weights, 790 with e4m3). All calls on one GPU share its
+ * array: calls that overlap in time there (other streams or threads) race
+ * and must be serialised by the caller. Every other error as for
+ * moe_grouped_ffn; FG_ERR_HIP if the device or the array's address cannot
+ * be queried.
+ */
+fg_status moe_grouped_ffn_noalloc(const moe_desc *d, const void *tokens,
+                                  const float *router_logits, const void *w_gateup,
+                                  const void *w_down, const float *s_gateup,
+                                  const float *s_down, void *out, int32_t *topk_idx,
+                                  float *topk_w, int32_t *perm, int32_t *expert_offsets,
+                                  void *stream);
+
+/* Bytes of the static scratch moe_grouped_ffn_noalloc uses on each GPU. */
+size_t moe_noalloc_scratch_bytes(void);
+
+/*
  * moe_finalize — the MoE finalize step on its own (paper §IV-A, the "MoE
  * finalize" kernel of Table I; also the last launch of moe_grouped_ffn):
  *   out[t, :] = Σ_{j = 0 .. top_k−1} y_slot[t·top_k + j, :]

@@ -81,6 +81,10 @@ def lib():
         L.moe_workspace_bytes.restype = sz
         L.moe_grouped_ffn.argtypes = [C.POINTER(MoeDesc)] + [vp] * 12 + [sz, vp]
         L.moe_grouped_ffn.restype = i32
+        L.moe_grouped_ffn_noalloc.argtypes = [C.POINTER(MoeDesc)] + [vp] * 12
+        L.moe_grouped_ffn_noalloc.restype = i32
+        L.moe_noalloc_scratch_bytes.argtypes = []
+        L.moe_noalloc_scratch_bytes.restype = sz
         L.moe_finalize.argtypes = [vp, vp, i64, i64, i32, vp]
         L.moe_finalize.restype = i32
         L.add_rmsnorm.argtypes = [vp, vp, vp, vp, i64, i64, C.c_float, vp]
@@ -218,6 +222,18 @@ def moe_grouped_ffn(desc, tokens, router_logits, w_gateup, w_down, s_gateup, s_d
                                s_down, out, topk_idx, topk_w, perm, expert_offsets, workspace,
                                ws_bytes, stream)
     _check(st, "moe_grouped_ffn")
+
+
+def moe_grouped_ffn_noalloc(desc, tokens, router_logits, w_gateup, w_down, s_gateup, s_down, out,
+                            topk_idx, topk_w, perm, expert_offsets, stream=None):
+    """moe_grouped_ffn with the library's static per-GPU scratch as workspace."""
+    st = lib().moe_grouped_ffn_noalloc(C.byref(desc), tokens, router_logits, w_gateup, w_down, s_gateup,
+                                       s_down, out, topk_idx, topk_w, perm, expert_offsets, stream)
+    _check(st, "moe_grouped_ffn_noalloc")
+
+
+def moe_noalloc_scratch_bytes():
+    return lib().moe_noalloc_scratch_bytes()
 
 
 def fg_quantize_rows_e4m3(x, rows, cols, q, s, stream=None):

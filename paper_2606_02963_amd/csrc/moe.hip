@@ -23,6 +23,7 @@
 #include <atomic>
 
 #include "fg_host.hpp"
+#include "fg_moe.hpp"
 #include "fg_quant.hpp"
 #include "fg_tile.hpp"
 #include "fgemm.h"
@@ -678,7 +679,7 @@ static MoeLayout layout(const moe_desc& d) {
   return L;
 }
 
-static fg_status validate_desc(const moe_desc* d, const char* fn) {
+fg_status validate_desc(const moe_desc* d, const char* fn) {
   if (d == nullptr) return fail(FG_ERR_INVALID_ARG, "%s: desc is NULL", fn);
   if (d->T < 0 || d->T > 0x7fffffffLL) return fail(FG_ERR_INVALID_ARG, "%s: bad T=%lld", fn, (long long)d->T);
   if (d->H <= 0 || d->I <= 0 || d->H > (1 << 20) || d->I > (1 << 20))
@@ -754,13 +755,12 @@ extern "C" size_t moe_workspace_bytes(const moe_desc* d) {
   return layout(*d).total;
 }
 
-extern "C" fg_status moe_grouped_ffn(const moe_desc* d, const void* tokens, const float* router_logits,
-                                     const void* w_gateup, const void* w_down, const float* s_gateup,
-                                     const float* s_down, void* out, int32_t* topk_idx, float* topk_w,
-                                     int32_t* perm, int32_t* expert_offsets, void* workspace, size_t ws_bytes,
-                                     void* stream) {
-  clear_error();
-  const char* fn = "moe_grouped_ffn";
+// The MoE step on a given workspace (the body of both entry points):
+// validates every argument, then enqueues the launches.
+fg_status fg::moe_run(const char* fn, const moe_desc* d, const void* tokens, const float* router_logits,
+                      const void* w_gateup, const void* w_down, const float* s_gateup, const float* s_down,
+                      void* out, int32_t* topk_idx, float* topk_w, int32_t* perm, int32_t* expert_offsets,
+                      void* workspace, size_t ws_bytes, void* stream) {
   fg_status st = validate_desc(d, fn);
   if (st != FG_OK) return st;
   const bool f8 = d->w_dtype == FG_E4M3;
@@ -866,6 +866,16 @@ extern "C" fg_status moe_grouped_ffn(const moe_desc* d, const void* tokens, cons
 
   lc.add(launch_finalize(reinterpret_cast<const float*>(ws + L.y), out, d->T, d->H, d->top_k, s));
   return check_launch(fn, lc);
+}
+
+extern "C" fg_status moe_grouped_ffn(const moe_desc* d, const void* tokens, const float* router_logits,
+                                     const void* w_gateup, const void* w_down, const float* s_gateup,
+                                     const float* s_down, void* out, int32_t* topk_idx, float* topk_w,
+                                     int32_t* perm, int32_t* expert_offsets, void* workspace, size_t ws_bytes,
+                                     void* stream) {
+  clear_error();
+  return moe_run("moe_grouped_ffn", d, tokens, router_logits, w_gateup, w_down, s_gateup, s_down, out, topk_idx,
+                 topk_w, perm, expert_offsets, workspace, ws_bytes, stream);
 }
 
 extern "C" fg_status moe_finalize(const void* y_slot, void* out, int64_t T, int64_t H, int32_t top_k, void* stream) {

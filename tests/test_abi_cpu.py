@@ -329,3 +329,22 @@ def test_trace_validation_without_gpu():
         with pytest.raises(L.FgError) as ei:
             L.fg_trace_read(i)
         assert ei.value.status == L.FG_ERR_INVALID_ARG
+
+
+def test_noalloc_moe_rejects_before_any_hip_call():
+    """moe_grouped_ffn_noalloc validates the descriptor and the scratch size
+    on the host: an invalid descriptor gives its usual status and a problem
+    larger than the static scratch FG_ERR_UNSUPPORTED, without a GPU."""
+    assert L.moe_noalloc_scratch_bytes() == 64 << 20
+    bad = L.moe_desc(8, 100, 64, 8, 2)                       # H not a multiple of 64
+    with pytest.raises(L.FgError) as ei:
+        L.moe_grouped_ffn_noalloc(bad, *([1 << 40] * 11), None)
+    assert ei.value.status == L.FG_ERR_ALIGNMENT
+    big = L.moe_desc(4096, 2880, 2880, 32, 4)                # the prefill step needs ~290 MB
+    assert L.moe_workspace_bytes(big) > L.moe_noalloc_scratch_bytes()
+    with pytest.raises(L.FgError) as ei:
+        L.moe_grouped_ffn_noalloc(big, *([1 << 40] * 11), None)
+    assert ei.value.status == L.FG_ERR_UNSUPPORTED
+    assert "static scratch" in str(ei.value)
+    fits = L.moe_desc(900, 2880, 2880, 32, 4)
+    assert L.moe_workspace_bytes(fits) <= L.moe_noalloc_scratch_bytes()

@@ -1,0 +1,74 @@
+"""The allocation-free MoE entry point (moe_grouped_ffn_noalloc) against the
+workspace entry point (moe_grouped_ffn), through the C ABI.
+
+Both run the same kernels on the same inputs, so every output must agree
+bit for bit: token outputs, top-k indices and weights, the permutation and
+the expert offsets. Each case makes two calls in a row on the static
+scratch, the second with fewer tokens (and the other row-tile size), so
+that anything a call depends on from the scratch's previous contents would
+show up. The smaller call is also checked against the fp64 oracle."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import bf16_decode, compare, e4m3_decode, ref_moe
+from paper_2606_02963_amd import _lib as L
+from paper_2606_02963_amd import api
+from paper_2606_02963_amd.synth import MoeSpec, make_moe_activations, make_moe_weights
+from tests.gpu_helpers import dev_bf16, dev_f32, dev_u8, host64, log, require_gpu
+
+pytestmark = pytest.mark.gpu
+
+
+def _noalloc(desc, x, lg, wgu, wd, sgu, sd):
+    T, k, E, H = desc.T, desc.top_k, desc.E, desc.H
+    dev = x.device
+    out = torch.full((T, H), float("nan"), dtype=torch.bfloat16, device=dev)
+    idx = torch.full((T, k), -1, dtype=torch.int32, device=dev)
+    w = torch.full((T, k), float("nan"), dtype=torch.float32, device=dev)
+    perm = torch.full((T * k,), -1, dtype=torch.int32, device=dev)
+    offs = torch.full((E + 1,), -1, dtype=torch.int32, device=dev)
+    p = lambda t: t.data_ptr() if t is not None else None  # noqa: E731
+    L.moe_grouped_ffn_noalloc(desc, p(x), p(lg), p(wgu), p(wd), p(sgu), p(sd), p(out), p(idx), p(w), p(perm),
+                              p(offs), torch.cuda.current_stream().cuda_stream)
+    return out, idx, w, perm, offs
+
+
+@pytest.mark.parametrize("w_dtype,T1,T2", [("bf16", 300, 40), ("e4m3", 256, 9)])
+def test_noalloc_matches_workspace_entry_point(w_dtype, T1, T2):
+    require_gpu()
+    base = MoeSpec(f"noalloc_{w_dtype}", T=T1, H=2880, I=2880, E=8, k=4, w_dtype=w_dtype)
+    w = make_moe_weights(base, 31)
+    if w_dtype == "bf16":
+        wgu, wd, sgu, sd = dev_bf16(w["w_gate_up"]), dev_bf16(w["w_down"]), None, None
+    else:
+        wgu, wd = dev_u8(w["w_gate_up"]), dev_u8(w["w_down"])
+        sgu, sd = dev_f32(w["s_gate_up"]), dev_f32(w["s_down"])
+    for T in (T1, T2):
+        spec = MoeSpec(base.name, T=T, H=base.H, I=base.I, E=base.E, k=base.k, w_dtype=w_dtype)
+        log(f"[noalloc] {w_dtype} T={T} H={spec.H} I={spec.I} E={spec.E} k={spec.k}")
+        act = make_moe_activations(spec, 32 + T)
+        x, lg = dev_bf16(act["x"]), dev_f32(act["logits"])
+        desc = L.moe_desc(T, spec.H, spec.I, spec.E, spec.k, w_dtype)
+        assert L.moe_workspace_bytes(desc) <= L.moe_noalloc_scratch_bytes()
+        ref_run = api.moe_ffn(x, lg, wgu, wd, sgu, sd, top_k=spec.k)
+        got = _noalloc(desc, x, lg, wgu, wd, sgu, sd)
+        torch.cuda.synchronize()
+        assert torch.equal(got[0].view(torch.int16), ref_run.out.view(torch.int16)), "token outputs differ"
+        assert torch.equal(got[1], ref_run.topk_idx)
+        assert torch.equal(got[2].view(torch.int32), ref_run.topk_w.view(torch.int32))
+        assert torch.equal(got[3], ref_run.perm)
+        assert torch.equal(got[4], ref_run.offsets)
+    # the second (smaller) call against the oracle as well
+    f8 = w_dtype == "e4m3"
+    if f8:
+        W = lambda e: (e4m3_decode(w["w_gate_up"][e]) * w["s_gate_up"][e][:, None].astype(np.float64),  # noqa: E731
+                       e4m3_decode(w["w_down"][e]) * w["s_down"][e][:, None].astype(np.float64))
+    else:
+        W = lambda e: (bf16_decode(w["w_gate_up"][e]), bf16_decode(w["w_down"][e]))  # noqa: E731
+    ref = ref_moe(bf16_decode(act["x"]), act["logits"].astype(np.float64), W, spec.k,
+                  storage="e4m3" if f8 else "bf16", act_quant=f8, with_bound=True)
+    rep = compare(host64(got[0]), ref["out"], "e4m3" if f8 else "bf16", slack=ref["out_bound"])
+    log(f"    {rep}")
+    assert rep.ok, rep
