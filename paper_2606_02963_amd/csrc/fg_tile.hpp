@@ -487,44 +487,4 @@ __device__ __forceinline__ void store_tile_bf16(char* lds, Vals vals, RowPtr row
 }
 
 
-// fp32 variant of store_tile_bf16 for outputs kept in fp32 (the MoE per-slot
-// outputs). The tile goes through LDS in PASSES column slabs of OUTC/PASSES
-// columns, so a slab of a large tile fits in the LDS its main loop already
-// uses; each slab is written with 16-byte row-contiguous stores. `vals` as
-// for store_tile_bf16 (c within [0, OUTC)); `ncols` a multiple of 4. `lds`
-// needs BM·(4·OUTC/PASSES + 16) bytes.
-template <class TL, int OUTC, int PASSES, class Vals, class RowPtr>
-__device__ __forceinline__ void store_tile_f32(char* lds, Vals vals, RowPtr row_ptr, int ncols) {
-  static_assert(OUTC % (4 * PASSES) == 0, "slabs must hold whole 16-byte chunks");
-  constexpr int PC = OUTC / PASSES;   // columns per slab
-  constexpr int PITCH = PC * 4 + 16;
-  constexpr int CPR = PC / 4;         // 16-byte chunks per slab row
-  constexpr int TOTAL = TL::BM * CPR;
-#pragma unroll
-  for (int pass = 0; pass < PASSES; ++pass) {
-    __syncthreads();
-#pragma unroll
-    for (int fm = 0; fm < TL::FM; ++fm)
-#pragma unroll
-      for (int fn = 0; fn < TL::FN; ++fn)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          float v;
-          int c;
-          if (vals(fm, fn, i, v, c) && c >= pass * PC && c < (pass + 1) * PC) {
-            const int r = acc_row<TL>(fm, i);
-            *reinterpret_cast<float*>(lds + r * PITCH + (c - pass * PC) * 4) = v;
-          }
-        }
-    __syncthreads();
-    for (int idx = threadIdx.x; idx < TOTAL; idx += TL::THREADS) {
-      const int r = idx / CPR, c = idx % CPR;
-      const int col = pass * PC + c * 4;
-      char* dst = row_ptr(r);
-      if (dst != nullptr && col < ncols)
-        *reinterpret_cast<i32x4*>(dst + col * 4) = *reinterpret_cast<const i32x4*>(lds + r * PITCH + c * 16);
-    }
-  }
-}
-
 }  // namespace fg
