@@ -96,6 +96,24 @@ def test_parity_small(spec):
     run_spec(spec)
 
 
+# Row LogSumExp at small M (the 16 / 64 / 256-row shapes of the one-launch
+# comparison, N = 8192, K = 4096, split-K), ragged rows and columns, one
+# partial n-tile, and a post op.
+LSE_SMALL_M = [
+    C3.scaled(M=16, N=8192, K=4096),
+    C3.scaled(M=64, N=8192, K=4096),
+    C3.scaled(M=256, N=8192, K=4096),
+    C3.scaled(M=5, N=1000, K=264),
+    C3.scaled(M=33, N=96, K=64),
+    FGEMM_SPECS["bf16_scale_lse_mish"].scaled(M=250, N=1000, K=264),
+]
+
+
+@pytest.mark.parametrize("spec", LSE_SMALL_M, ids=lambda s: s.name)
+def test_parity_lse_small_m(spec):
+    run_spec(spec)
+
+
 # Table III tail chains: Mish, LeakyReLU and elementwise ops after the
 # reduction, on every tile configuration and after a split-K gather.
 T3 = [FGEMM_SPECS[k] for k in ("bf16_scale_lse_mish", "bf16_gn_swish_mul_swish", "bf16_gn_lrelu_sum",
