@@ -121,16 +121,20 @@ typedef struct fg_plan fg_plan; /* opaque, host memory, immutable once built */
  *   out_dtype FG_F32 or FG_BF16; LogSumExp requires FG_F32. N must be a
  *            multiple of 4 (f32 out) or 8 (bf16 out) (FG_ERR_ALIGNMENT).
  *   epi      the tail (copied into the plan; the caller keeps ownership).
- *            GroupNorm is supported for group widths N/gn_groups of 64 or
- *            128 channels (FG_ERR_UNSUPPORTED otherwise).
+ *            GroupNorm accepts any gn_groups that divides N. Groups of
+ *            16, 32, 64 or 128 channels (and 256 with bf16 inputs) are
+ *            normalised inside the GEMM launch; other widths take a second
+ *            launch, and the workspace then holds the fp32 values before
+ *            the normalisation (M·N·4 bytes).
  */
 fg_status fgemm_plan(fg_plan **plan, int64_t M, int64_t N, int64_t K,
                      int32_t in_dtype, int32_t out_dtype, const fg_epilogue *epi);
 
 /* Bytes of device workspace fgemm_run needs: the LogSumExp per-tile
- * (max, Σexp) pairs, and, when the plan splits K across workgroups, one
- * arrival counter per output tile plus an fp32 partial tile per slice. 0 when
- * neither applies, and for a NULL plan. */
+ * (max, Σexp) pairs, or the fp32 pre-normalisation values of a GroupNorm
+ * that takes a second launch, and, when the plan splits K across
+ * workgroups, one arrival counter per output tile plus an fp32 partial tile
+ * per slice. 0 when none applies, and for a NULL plan. */
 size_t fgemm_workspace_bytes(const fg_plan *plan);
 
 /*

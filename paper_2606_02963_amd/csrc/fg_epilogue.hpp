@@ -175,13 +175,87 @@ __device__ __forceinline__ void lse_partials(f32x4 (&acc)[TL::FM][TL::FN], float
   }
 }
 
-// GroupNorm inside the tile. Group width gw is a multiple of the wave tile
-// width TN and divides BN, so each wave's columns lie in one group and a
-// group's statistics are the sum over the waves whose columns it covers.
-// `red` needs WN·BM floats of LDS.
+// Sum over the 16 lanes of a DPP row that every lane receives bit for bit:
+// quad_perm [1,0,3,2] and [2,3,0,1], then row_half_mirror and row_mirror
+// pair each lane with a partner holding the same partial sums in the same
+// association, so the final value does not depend on the lane.
+__device__ __forceinline__ float row16_sum_uniform(float v) {
+  v += dpp_f<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_f<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_f<0x141>(v);  // row_half_mirror
+  v += dpp_f<0x140>(v);  // row_mirror
+  return v;
+}
+
+// GroupNorm over groups of FPG whole 16-column fragments of one wave
+// (gw = 16·FPG ≤ TN): each group's mean, then its biased variance about the
+// mean, from the wave's registers with one 16-lane reduction per row and
+// group; then the normalisation and the per-channel affine map.
+template <class TL, int FPG>
+__device__ __forceinline__ void groupnorm_inwave(f32x4 (&acc)[TL::FM][TL::FN], int n0, int N, float eps,
+                                                 const float* gamma, const float* beta) {
+  static_assert(TL::FN % FPG == 0, "a group must be whole fragments of one wave");
+  constexpr float inv_gw = 1.0f / (16.0f * FPG);
+  float gm[TL::FN], bt[TL::FN];
+#pragma unroll
+  for (int fn = 0; fn < TL::FN; ++fn) {
+    const int n = n0 + acc_col<TL>(fn);
+    gm[fn] = n < N ? gamma[n] : 0.0f;
+    bt[fn] = n < N ? beta[n] : 0.0f;
+  }
+#pragma unroll
+  for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int q = 0; q < TL::FN / FPG; ++q) {
+        float sm = 0.0f;
+#pragma unroll
+        for (int f = 0; f < FPG; ++f) sm += acc[fm][q * FPG + f][i];
+        const float mu = row16_sum_uniform(sm) * inv_gw;
+        float sq = 0.0f;
+#pragma unroll
+        for (int f = 0; f < FPG; ++f) {
+          const float d = acc[fm][q * FPG + f][i] - mu;
+          sq += d * d;
+        }
+        const float rstd = fast_rsqrt(row16_sum_uniform(sq) * inv_gw + eps);
+#pragma unroll
+        for (int f = 0; f < FPG; ++f) {
+          const int fn = q * FPG + f;
+          acc[fm][fn][i] = (acc[fm][fn][i] - mu) * rstd * gm[fn] + bt[fn];
+        }
+      }
+}
+
+// Whether a tile can normalise groups of gw channels in registers: gw a
+// multiple of 16 that either divides the wave tile width (a group is whole
+// fragments of one wave) or is a multiple of it that divides the tile width
+// (a group is whole wave columns).
+template <class TL>
+constexpr bool groupnorm_fits_tile(int gw) {
+  return gw % 16 == 0 && (gw <= TL::TN ? TL::TN % gw == 0 : (gw % TL::TN == 0 && TL::BN % gw == 0));
+}
+
+// GroupNorm inside the tile, for groups that groupnorm_fits_tile accepts.
+// Groups of at most one wave's width are handled by groupnorm_inwave; wider
+// groups span whole wave columns, and their statistics are the sum over the
+// waves whose columns they cover (exchanged through `red`, WN·BM floats of
+// LDS). Both take the mean first and then the biased variance about it.
 template <class TL>
 __device__ __forceinline__ void groupnorm_tile(f32x4 (&acc)[TL::FM][TL::FN], float* red, int n0, int N,
                                                int gw, float eps, const float* gamma, const float* beta) {
+  static_assert(TL::FN == 4, "the in-wave group sizes below assume 64-column wave tiles");
+  if (gw <= TL::TN) {
+    // 16, 32 or 64 channels (the host admits no other width here)
+    if (gw == 16)
+      groupnorm_inwave<TL, 1>(acc, n0, N, eps, gamma, beta);
+    else if (gw == 32)
+      groupnorm_inwave<TL, 2>(acc, n0, N, eps, gamma, beta);
+    else
+      groupnorm_inwave<TL, 4>(acc, n0, N, eps, gamma, beta);
+    return;
+  }
   const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
   const int wn = wave % TL::WN;
   const int my_group = (wn * TL::TN) / gw;

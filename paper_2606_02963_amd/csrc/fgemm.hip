@@ -272,6 +272,48 @@ __global__ __launch_bounds__(256) void lse_combine_kernel(const float2* ws, floa
   }
 }
 
+// GroupNorm of groups that no tile holds in registers (wider than the tile,
+// or not whole 16-column fragments): the GEMM launch has written the fp32
+// pre-normalisation values z [M, N] (bias and ops applied) to the workspace,
+// and this launch normalises them. One workgroup per row, one wave per group
+// at a time: the group's mean, then its biased variance about the mean
+// (each a wave-wide sum whose butterfly leaves the same value in every
+// lane), then (z − μ)/√(σ² + eps)·γ + β, the post ops, and the store.
+__global__ __launch_bounds__(256) void groupnorm_rows_kernel(const float* z, void* out, int out_bf16, int64_t N,
+                                                             int gw, float eps, const float* gamma,
+                                                             const float* beta, EpiArgs post) {
+  const int64_t row = blockIdx.x;
+  const int wave = threadIdx.x >> 6, l = threadIdx.x & 63;
+  const float* zr = z + row * N;
+  const int groups = (int)(N / gw);
+  const float inv_gw = 1.0f / (float)gw;
+  for (int g = wave; g < groups; g += 4) {
+    const float* zg = zr + (int64_t)g * gw;
+    float s = 0.0f;
+    for (int j = l; j < gw; j += 64) s += zg[j];
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) s += __shfl_xor(s, m, 64);
+    const float mu = s * inv_gw;
+    float q = 0.0f;
+    for (int j = l; j < gw; j += 64) {
+      const float d = zg[j] - mu;
+      q += d * d;
+    }
+#pragma unroll
+    for (int m = 1; m < 64; m <<= 1) q += __shfl_xor(q, m, 64);
+    const float rstd = fast_rsqrt(q * inv_gw + eps);
+    for (int j = l; j < gw; j += 64) {
+      const int64_t n = (int64_t)g * gw + j;
+      float v = (zg[j] - mu) * rstd * gamma[n] + beta[n];
+      for (int o = 0; o < post.n_ops; ++o) v = apply_op_scalar(post.kind[o], post.a[o], post.b[o], v);
+      if (out_bf16)
+        static_cast<uint16_t*>(out)[row * N + n] = f32_to_bf16_bits(v);
+      else
+        static_cast<float*>(out)[row * N + n] = v;
+    }
+  }
+}
+
 // ---------------------------------------------------------------------------
 // kernel table
 
@@ -297,6 +339,24 @@ struct TileModel {
   int cfg, BM, BN;
   double eff;
 };
+
+// Tile width and wave tile width of each configuration (host copies of the
+// Tile parameters above), and the host twin of groupnorm_fits_tile.
+static void cfg_widths(int cfg, int& BN, int& TN) {
+  switch (cfg) {
+    case CFG_F32: BN = TileF32::BN; TN = TileF32::TN; break;
+    case CFG_BF16_256x256: BN = TileHuge::BN; TN = TileHuge::TN; break;
+    case CFG_BF16_256x128: BN = TileBig::BN; TN = TileBig::TN; break;
+    case CFG_BF16_128x128: BN = TileMid::BN; TN = TileMid::TN; break;
+    case CFG_E4M3_256x128: BN = TileF8Big::BN; TN = TileF8Big::TN; break;
+    default: BN = TileF8Mid::BN; TN = TileF8Mid::TN; break;
+  }
+}
+static bool groupnorm_in_tile(int cfg, int64_t gw) {
+  int BN, TN;
+  cfg_widths(cfg, BN, TN);
+  return gw % 16 == 0 && (gw <= TN ? TN % gw == 0 : (gw % TN == 0 && BN % gw == 0));
+}
 static const TileModel kBf16Tiles[] = {
     {CFG_BF16_256x256, 256, 256, 1.00},
     {CFG_BF16_256x128, 256, 128, 0.88},
@@ -347,6 +407,8 @@ struct fg_plan {
   int64_t kslice;           // bytes per row per slice (all but the last)
   int64_t tiles_m, tiles_n;
   size_t lse_bytes;         // LogSumExp pairs at the start of the workspace
+  int gn_two_pass;          // GroupNorm groups no tile holds: fp32 z in the workspace, second launch
+  size_t z_bytes;           // that z [M, N] at the start of the workspace
   size_t cnt_off, part_off; // split-K counters and partial tiles
   size_t ws_bytes;
 };
@@ -415,16 +477,14 @@ extern "C" fg_status fgemm_plan(fg_plan** plan, int64_t M, int64_t N, int64_t K,
     if (N % opc != 0)
       return fail(FG_ERR_ALIGNMENT, "fgemm_plan: N=%lld must be a multiple of %d", (long long)N, opc);
   }
-  int gw = 0;
+  int64_t gw = 0;
   if (red == FG_RED_GROUPNORM) {
     if (epi->gn_groups <= 0 || N % epi->gn_groups != 0)
       return fail(FG_ERR_INVALID_ARG, "fgemm_plan: N=%lld not divisible into %d groups", (long long)N,
                   epi->gn_groups);
     if (!(epi->gn_eps >= 0.0f) || !isfinite(epi->gn_eps))
       return fail(FG_ERR_INVALID_ARG, "fgemm_plan: gn_eps must be finite and >= 0");
-    gw = (int)(N / epi->gn_groups);
-    if (gw != 64 && gw != 128)
-      return fail(FG_ERR_UNSUPPORTED, "fgemm_plan: GroupNorm group width %d (supported: 64, 128)", gw);
+    gw = N / epi->gn_groups;
   }
 
   fg_plan* p = new (std::nothrow) fg_plan();
@@ -481,6 +541,18 @@ extern "C" fg_status fgemm_plan(fg_plan** plan, int64_t M, int64_t N, int64_t K,
       }
     }
   }
+  // GroupNorm: widths of 256 channels need the 256-column tile; groups no
+  // tile holds in registers take the second launch
+  p->gn_two_pass = 0;
+  if (red == FG_RED_GROUPNORM && !groupnorm_in_tile(p->cfg, gw)) {
+    if (in_dtype == FG_BF16 && groupnorm_in_tile(CFG_BF16_256x256, gw)) {
+      p->cfg = CFG_BF16_256x256;
+      p->BM = TileHuge::BM;
+      p->BN = TileHuge::BN;
+    } else {
+      p->gn_two_pass = 1;
+    }
+  }
   p->tiles_m = (M + p->BM - 1) / p->BM;
   p->tiles_n = (N + p->BN - 1) / p->BN;
   if (p->tiles_m * p->tiles_n > LIM) {
@@ -490,6 +562,8 @@ extern "C" fg_status fgemm_plan(fg_plan** plan, int64_t M, int64_t N, int64_t K,
   const int64_t stages = K * esize / 128;
   p->kslice = p->ks > 1 ? (stages / p->ks) * 128 : 0;
   p->lse_bytes = red == FG_RED_LOGSUMEXP_ROW ? (size_t)M * (size_t)p->tiles_n * sizeof(float2) : 0;
+  p->z_bytes = p->gn_two_pass ? (size_t)M * (size_t)N * sizeof(float) : 0;
+  if (p->z_bytes > 0) p->lse_bytes = p->z_bytes;   // the workspace's first region holds z instead
   p->cnt_off = round256(p->lse_bytes);
   p->part_off = p->cnt_off;
   p->ws_bytes = p->lse_bytes;
@@ -514,7 +588,7 @@ extern "C" fg_status fgemm_plan_info(const fg_plan* plan, int32_t* tile_m, int32
   if (tile_n) *tile_n = plan->BN;
   if (workgroups) *workgroups = plan->M == 0 ? 0 : plan->tiles_m * plan->tiles_n * plan->ks;
   if (launches)
-    *launches = plan->M == 0 ? 0 : (plan->epi.reduction == FG_RED_LOGSUMEXP_ROW ? 2 : 1);
+    *launches = plan->M == 0 ? 0 : (plan->epi.reduction == FG_RED_LOGSUMEXP_ROW || plan->gn_two_pass ? 2 : 1);
   if (k_slices) *k_slices = plan->ks;
   return FG_OK;
 }
@@ -579,21 +653,29 @@ static fg_status run_plan(const fg_plan* plan, const void* A, const void* W, con
     post.a[i] = p.epi.post_ops[i].a;
     post.b[i] = p.epi.post_ops[i].b;
   }
-  const int out_k = p.out_dt == FG_BF16 ? OUT_BF16 : OUT_F32;
+  // two-pass GroupNorm: the GEMM launch writes fp32 z (bias and ops
+  // applied) to the workspace as a plain fp32 output
+  const int kred = p.gn_two_pass ? FG_RED_NONE : red;
+  const int out_k = p.gn_two_pass ? OUT_F32 : (p.out_dt == FG_BF16 ? OUT_BF16 : OUT_F32);
+  if (p.gn_two_pass) a.out = workspace;
   KernelChoice kc{nullptr, 0};
   switch (p.cfg) {
-    case CFG_F32: kc = pick_kernel<TileF32>(red, out_k); break;
-    case CFG_BF16_256x256: kc = pick_kernel<TileHuge>(red, out_k); break;
-    case CFG_BF16_256x128: kc = pick_kernel<TileBig>(red, out_k); break;
-    case CFG_BF16_128x128: kc = pick_kernel<TileMid>(red, out_k); break;
-    case CFG_E4M3_256x128: kc = pick_kernel<TileF8Big>(red, out_k); break;
-    case CFG_E4M3_128x128: kc = pick_kernel<TileF8Mid>(red, out_k); break;
+    case CFG_F32: kc = pick_kernel<TileF32>(kred, out_k); break;
+    case CFG_BF16_256x256: kc = pick_kernel<TileHuge>(kred, out_k); break;
+    case CFG_BF16_256x128: kc = pick_kernel<TileBig>(kred, out_k); break;
+    case CFG_BF16_128x128: kc = pick_kernel<TileMid>(kred, out_k); break;
+    case CFG_E4M3_256x128: kc = pick_kernel<TileF8Big>(kred, out_k); break;
+    case CFG_E4M3_128x128: kc = pick_kernel<TileF8Mid>(kred, out_k); break;
   }
   if (kc.fn == nullptr) return fail(FG_ERR_UNSUPPORTED, "fgemm_run: no kernel for this plan");
   hipStream_t s = static_cast<hipStream_t>(stream);
   const unsigned grid = (unsigned)(p.tiles_m * p.tiles_n * p.ks);
   Launches lc;
   lc.add(launch(kc.fn, dim3(grid), dim3(kc.threads), 0, s, a, ep, post));
+  if (p.gn_two_pass)
+    lc.add(launch(groupnorm_rows_kernel, dim3((unsigned)p.M), dim3(256), 0, s,
+                  static_cast<const float*>(workspace), out, p.out_dt == FG_BF16 ? 1 : 0, p.N,
+                  (int)(p.N / p.epi.gn_groups), p.epi.gn_eps, gamma, beta, post));
   if (red == FG_RED_LOGSUMEXP_ROW) {
     const unsigned g2 = (unsigned)((p.M + 3) / 4);
     lc.add(launch(lse_combine_kernel, dim3(g2), dim3(256), 0, s, a.ws, static_cast<float*>(out), (int)p.M,

@@ -87,7 +87,8 @@ def test_plan_validation_statuses():
     gn = dict(reduction="groupnorm", gn_groups=32, gn_eps=1e-5)
     assert plan_status(8, 4096, 256, "bf16", "bf16", E(**gn)) == L.FG_OK      # width 128
     assert plan_status(8, 2048, 256, "bf16", "bf16", E(**gn)) == L.FG_OK      # width 64
-    assert plan_status(8, 1024, 256, "bf16", "bf16", E(**gn)) == L.FG_ERR_UNSUPPORTED  # width 32
+    assert plan_status(8, 1024, 256, "bf16", "bf16", E(**gn)) == L.FG_OK      # width 32
+    assert plan_status(8, 4000, 256, "bf16", "bf16", E(**gn)) == L.FG_OK      # width 125 (second launch)
     assert plan_status(8, 4008, 256, "bf16", "bf16", E(**gn)) == L.FG_ERR_INVALID_ARG  # not divisible
     gn_neg = E(reduction="groupnorm", gn_groups=32, gn_eps=-1.0)
     assert plan_status(8, 4096, 256, "bf16", "bf16", gn_neg) == L.FG_ERR_INVALID_ARG
@@ -119,6 +120,27 @@ def test_last_error_describes_the_failure():
     with pytest.raises(L.FgError) as ei:
         L.fgemm_plan(8, 256, 260, "bf16", "bf16", E())
     assert "K=260" in str(ei.value) and "multiple of 8" in L.last_error()
+
+
+def test_groupnorm_group_widths():
+    """Any width that divides N is accepted. Widths of 16, 32 and 64
+    channels run inside the tile (one launch, no workspace), 256 on the
+    256×256 tile; widths no tile holds in registers take a second launch with
+    an fp32 workspace of M·N values."""
+    def gn(M, N, groups, dt="bf16"):
+        p = L.fgemm_plan(M, N, 256, dt, "bf16", E(reduction="groupnorm", gn_groups=groups, gn_eps=1e-5))
+        return p.info(), p.workspace_bytes()
+    for groups in (32, 16, 8, 4):                       # 16, 32, 64, 128 channels
+        i, ws = gn(300, 512, groups)
+        assert i["launches"] == 1 and ws == 0, groups
+    i, ws = gn(512, 2048, 8)                            # 256 channels
+    assert (i["tile_m"], i["tile_n"], i["launches"], ws) == (256, 256, 1, 0)
+    for M, N, groups in ((300, 4096, 8), (130, 480, 20), (77, 384, 4), (130, 4096, 1)):
+        i, ws = gn(M, N, groups)
+        assert i["launches"] == 2 and ws == M * N * 4, (M, N, groups)
+    i, ws = gn(256, 2048, 8, "e4m3")                   # no e4m3 tile holds 256 channels
+    assert i["launches"] == 2 and ws == 256 * 2048 * 4
+    assert plan_status(8, 480, 256, "bf16", "bf16", E(reduction="groupnorm", gn_groups=7)) == L.FG_ERR_INVALID_ARG
 
 
 def test_tile_choice_and_workspace():

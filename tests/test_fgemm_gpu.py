@@ -114,6 +114,39 @@ def test_parity_lse_small_m(spec):
     run_spec(spec)
 
 
+# GroupNorm over every kind of group width: 16 and 32 channels inside one
+# wave, 64 inside one wave on the 256×256 tile too, 256 channels on the
+# 256×256 tile (across its four wave columns), and groups no tile holds in
+# registers — wider than the tile (512, 2048), or not whole 16-column
+# fragments (24, 96) — through the second launch, with post ops, e4m3 and
+# fp32 inputs and fp32 output.
+_SILU = (("silu",),)
+GN_WIDTHS = [
+    FgemmSpec("gn16", 300, 512, 264, "bf16", 1 / 16, _SILU, "groupnorm", 32, 1e-5),
+    FgemmSpec("gn32", 200, 1024, 136, "bf16", 1 / 16, _SILU, "groupnorm", 32, 1e-5),
+    FgemmSpec("gn64_huge", 4000, 4096, 200, "bf16", 1 / 16, _SILU, "groupnorm", 64, 1e-5),
+    FgemmSpec("gn256", 512, 2048, 256, "bf16", 1 / 16, _SILU, "groupnorm", 8, 1e-5),
+    FgemmSpec("gn512_two_pass", 300, 4096, 264, "bf16", 1 / 16, _SILU, "groupnorm", 8, 1e-5,
+              post_ops=(("leaky_relu", 0.01), ("scale", 2.0))),
+    FgemmSpec("gn2048_two_pass", 130, 4096, 128, "bf16", 1 / 16, _SILU, "groupnorm", 2, 1e-5),
+    FgemmSpec("gn24_two_pass", 130, 480, 64, "bf16", 1 / 8, _SILU, "groupnorm", 20, 1e-5),
+    FgemmSpec("gn96_two_pass", 77, 384, 72, "bf16", 1 / 8, _SILU, "groupnorm", 4, 1e-5, out_dtype="f32"),
+    FgemmSpec("gn256_e4m3_two_pass", 256, 2048, 256, "e4m3", 1 / 16, _SILU, "groupnorm", 8, 1e-5),
+    FgemmSpec("gn16_f32", 96, 256, 64, "f32", 0.2, _SILU, "groupnorm", 16, 1e-5),
+    FgemmSpec("gn512_f32_two_pass", 96, 1024, 64, "f32", 0.2, _SILU, "groupnorm", 2, 1e-5),
+]
+
+
+@pytest.mark.parametrize("spec", GN_WIDTHS, ids=lambda s: s.name)
+def test_parity_groupnorm_widths(spec):
+    gw = spec.N // spec.gn_groups
+    plan = api.get_plan(spec.M, spec.N, spec.K, spec.dtype, spec.out, True, spec.ops, "groupnorm",
+                        spec.gn_groups, spec.gn_eps, spec.post_ops)
+    log(f"[gn] width {gw}: {plan.info()}")
+    assert plan.info()["launches"] == (2 if "two_pass" in spec.name else 1)
+    run_spec(spec)
+
+
 # Table III tail chains: Mish, LeakyReLU and elementwise ops after the
 # reduction, on every tile configuration and after a split-K gather.
 T3 = [FGEMM_SPECS[k] for k in ("bf16_scale_lse_mish", "bf16_gn_swish_mul_swish", "bf16_gn_lrelu_sum",
