@@ -56,6 +56,11 @@ struct Launches {
 // is not reported again to the next unrelated HIP user on the thread.
 fg_status check_launch(const char* what, const Launches& l);
 
+// Run epochs for the arrival words of K-split exchanges: distinct for every
+// launch of the process (0 is skipped), so a word left by any other launch
+// never matches.
+unsigned next_epoch();
+
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 }  // namespace fg

@@ -3,6 +3,7 @@
 #include <stdarg.h>
 #include <stdio.h>
 
+#include <atomic>
 #include <vector>
 
 #include "fg_host.hpp"
@@ -21,6 +22,13 @@ fg_status fail(fg_status st, const char* fmt, ...) {
 }
 
 void clear_error() { g_last_error[0] = '\0'; }
+
+static std::atomic<unsigned> g_epoch{0};
+unsigned next_epoch() {
+  unsigned e;
+  do e = g_epoch.fetch_add(1, std::memory_order_relaxed) + 1; while (e == 0);
+  return e;
+}
 
 fg_status check_launch(const char* what, const Launches& l) {
   if (l.first == hipSuccess) return FG_OK;

@@ -396,6 +396,80 @@ __device__ __forceinline__ void gemm_mainloop(const LA& ra, const LB& rb,
   __syncthreads();
 }
 
+// K-slice exchange of one output tile computed by `ks` workgroups, each over
+// a slice of K (split-K). Every slice stores its partial accumulator tile
+// with device-coherent (sc1) 16-byte stores (thread-major, so each wave's
+// stores are contiguous), waits until they are acknowledged and then counts
+// its arrival in the tile's 64-bit counter word (high half: the run's
+// epoch, low half: arrivals in that run) with an atomic compare-and-swap. An
+// arrival that finds another epoch — left by an earlier run, or whatever the
+// workspace held — starts the count at 1 for this run, so the workspace
+// needs no initialisation. The slice that brings the count to ks reads the
+// partials back with device-coherent loads and adds them in slice order (so
+// the sum does not depend on which slice arrives last), resets the count to
+// 0 under the same epoch (a captured graph replaying the launch with the
+// same epoch then starts clean) and returns true; the others return false.
+// Only the partials and the counter are shared, and both are accessed
+// device-coherently, so no cache-wide write-back or invalidation is needed.
+// `partials` holds ks partial tiles of FM·FN·THREADS 16-byte values; `flag`
+// is one word of LDS.
+template <class TL>
+__device__ __forceinline__ bool slice_gather(f32x4 (&acc)[TL::FM][TL::FN], f32x4* partials, int ks, int slice,
+                                             unsigned long long* counter, unsigned epoch, unsigned* flag) {
+  constexpr int NF = TL::FM * TL::FN;
+  constexpr uint32_t SLICE = NF * TL::THREADS * 16;   // bytes of one partial tile
+  const int tid = threadIdx.x;
+  const i32x4 rsrc = make_buffer_rsrc(partials, static_cast<uint32_t>(ks) * SLICE);
+  const uint32_t lane_off = static_cast<uint32_t>(tid) * 16;
+#pragma unroll
+  for (int fm = 0; fm < TL::FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < TL::FN; ++fn)
+      fg_raw_buffer_store_b128(__builtin_bit_cast(i32x4, acc[fm][fn]), rsrc,
+                               slice * SLICE + (fm * TL::FN + fn) * TL::THREADS * 16 + lane_off, 0, FG_CPOL_DEVICE);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  if (tid == 0) {
+    const unsigned long long ep = (unsigned long long)epoch << 32;
+    unsigned long long old = __hip_atomic_load(counter, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), want;
+    while (true) {
+      want = (old & 0xffffffff00000000ull) == ep ? old + 1 : ep | 1ull;
+      if (__hip_atomic_compare_exchange_strong(counter, &old, want, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
+                                               __HIP_MEMORY_SCOPE_AGENT))
+        break;
+    }
+    *flag = (unsigned)want;
+  }
+  __syncthreads();
+  if (*flag != (unsigned)ks) return false;
+  // read back one fragment row (FN loads) at a time: the memory clobber keeps
+  // the compiler from hoisting every load, whose destinations would not fit
+  // beside the accumulators
+#pragma unroll 1
+  for (int k = slice == 0 ? 1 : 0; k < ks; ++k) {
+#pragma unroll
+    for (int fm = 0; fm < TL::FM; ++fm) {
+      f32x4 v[TL::FN];
+#pragma unroll
+      for (int fn = 0; fn < TL::FN; ++fn)
+        v[fn] = __builtin_bit_cast(
+            f32x4, fg_raw_buffer_load_b128(rsrc, k * SLICE + (fm * TL::FN + fn) * TL::THREADS * 16 + lane_off, 0,
+                                           FG_CPOL_DEVICE));
+#pragma unroll
+      for (int fn = 0; fn < TL::FN; ++fn) {
+        if (k == 0)
+          acc[fm][fn] = v[fn];
+        else
+          acc[fm][fn] += v[fn];
+      }
+      asm volatile("" ::: "memory");
+    }
+  }
+  if (tid == 0) __hip_atomic_store(counter, (unsigned long long)epoch << 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  __syncthreads();
+  return true;
+}
+
 // Position of accumulator element (fm, fn, i) inside the workgroup tile.
 template <class TL>
 __device__ __forceinline__ int acc_row(int fm, int i) {

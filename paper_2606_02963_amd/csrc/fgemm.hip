@@ -83,79 +83,14 @@ __device__ __forceinline__ void tile_coords(int tile, int tiles_m, int tiles_n, 
   tn = local / rows;
 }
 
-// Split-K exchange. Every slice stores its partial tile with device-coherent
-// 16-byte stores (thread-major, so each wave's stores are contiguous), waits
-// until they are acknowledged and then counts its arrival in the tile's
-// 64-bit counter word (high half: the run's epoch, low half: arrivals in
-// that run) with an atomic compare-and-swap. An arrival that finds another
-// epoch — left by an earlier run, or whatever the workspace held — starts the
-// count at 1 for this run, so the workspace needs no initialisation. The
-// slice that brings the count to ks reads the partials back with
-// device-coherent loads and adds them in slice order (so the sum does not
-// depend on which slice arrives last), resets the count to 0 under the same
-// epoch (a captured graph replaying the launch with the same epoch then
-// starts clean) and returns true. Only the partials and the counter are
-// shared, and both are accessed device-coherently, so no cache-wide
-// write-back or invalidation is needed.
+// Split-K exchange (see slice_gather): the partial tiles of tile `tile` sit
+// at partials + tile·ks·(one partial tile), its counter at counters[tile].
 template <class TL>
 __device__ __forceinline__ bool split_k_gather(const DenseArgs& a, int tile, int ks,
                                                f32x4 (&acc)[TL::FM][TL::FN], unsigned* flag) {
   constexpr int NF = TL::FM * TL::FN;
-  constexpr uint32_t SLICE = NF * TL::THREADS * 16;   // bytes of one partial tile
-  const int tid = threadIdx.x;
-  const i32x4 rsrc = make_buffer_rsrc(a.partials + (size_t)tile * a.ks * NF * TL::THREADS,
-                                      static_cast<uint32_t>(a.ks) * SLICE);
-  const uint32_t lane_off = static_cast<uint32_t>(tid) * 16;
-#pragma unroll
-  for (int fm = 0; fm < TL::FM; ++fm)
-#pragma unroll
-    for (int fn = 0; fn < TL::FN; ++fn)
-      fg_raw_buffer_store_b128(__builtin_bit_cast(i32x4, acc[fm][fn]), rsrc,
-                               ks * SLICE + (fm * TL::FN + fn) * TL::THREADS * 16 + lane_off, 0, FG_CPOL_DEVICE);
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  if (tid == 0) {
-    unsigned long long* word = a.counters + tile;
-    const unsigned long long ep = (unsigned long long)a.epoch << 32;
-    unsigned long long old = __hip_atomic_load(word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT), want;
-    while (true) {
-      want = (old & 0xffffffff00000000ull) == ep ? old + 1 : ep | 1ull;
-      if (__hip_atomic_compare_exchange_strong(word, &old, want, __ATOMIC_RELAXED, __ATOMIC_RELAXED,
-                                               __HIP_MEMORY_SCOPE_AGENT))
-        break;
-    }
-    *flag = (unsigned)want;
-  }
-  __syncthreads();
-  if (*flag != (unsigned)a.ks) return false;
-  // read back one fragment row (FN loads) at a time: the memory clobber keeps
-  // the compiler from hoisting every load, whose destinations would not fit
-  // beside the accumulators
-#pragma unroll 1
-  for (int k = ks == 0 ? 1 : 0; k < a.ks; ++k) {
-#pragma unroll
-    for (int fm = 0; fm < TL::FM; ++fm) {
-      f32x4 v[TL::FN];
-#pragma unroll
-      for (int fn = 0; fn < TL::FN; ++fn)
-        v[fn] = __builtin_bit_cast(
-            f32x4, fg_raw_buffer_load_b128(rsrc, k * SLICE + (fm * TL::FN + fn) * TL::THREADS * 16 + lane_off, 0,
-                                           FG_CPOL_DEVICE));
-#pragma unroll
-      for (int fn = 0; fn < TL::FN; ++fn) {
-        if (k == 0)
-          acc[fm][fn] = v[fn];
-        else
-          acc[fm][fn] += v[fn];
-      }
-      asm volatile("" ::: "memory");
-    }
-  }
-  if (tid == 0)
-    __hip_atomic_store(a.counters + tile, (unsigned long long)a.epoch << 32, __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_AGENT);
-  __syncthreads();
-  return true;
+  return slice_gather<TL>(acc, a.partials + (size_t)tile * a.ks * NF * TL::THREADS, a.ks, ks, a.counters + tile,
+                          a.epoch, flag);
 }
 
 template <class TL, int RED, int OUT>
@@ -415,14 +350,7 @@ struct fg_plan {
 
 static size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Split-K run epochs: distinct for every run of the process (0 is skipped),
-// so a counter word left by any other run never matches.
-static std::atomic<unsigned> g_epoch{0};
-static unsigned next_epoch() {
-  unsigned e;
-  do e = g_epoch.fetch_add(1, std::memory_order_relaxed) + 1; while (e == 0);
-  return e;
-}
+
 
 extern "C" fg_status fgemm_plan(fg_plan** plan, int64_t M, int64_t N, int64_t K, int32_t in_dtype,
                                 int32_t out_dtype, const fg_epilogue* epi) {

@@ -40,15 +40,23 @@ def _dev_weights(spec, w):
             dev_f32(w["s_down"]))
 
 
-def run_moe(spec, seed=0, act=None, w=None, tokens=None, interleaved=False, check_out=True):
+def run_moe(spec, seed=0, act=None, w=None, tokens=None, interleaved=False, check_out=True, repeat=False):
     require_gpu()
     log(f"[moe] {spec.name} T={spec.T} H={spec.H} I={spec.I} E={spec.E} k={spec.k} {spec.w_dtype} seed={seed}")
     act = act if act is not None else make_moe_activations(spec, seed)
     w = w if w is not None else make_moe_weights(spec, seed)
     wgu, wd, sgu, sd = _dev_weights(spec, w)
-    res = api.moe_ffn(dev_bf16(act["x"]), dev_f32(act["logits"]), wgu, wd, sgu, sd, top_k=spec.k,
-                      alpha=spec.alpha, limit=spec.limit, interleaved=interleaved)
+    x, lg = dev_bf16(act["x"]), dev_f32(act["logits"])
+    res = api.moe_ffn(x, lg, wgu, wd, sgu, sd, top_k=spec.k, alpha=spec.alpha, limit=spec.limit,
+                      interleaved=interleaved)
     torch.cuda.synchronize()
+    if repeat:
+        # a second step on a fresh workspace: the same bits (K-split exchanges
+        # add their partial tiles in a fixed order)
+        again = api.moe_ffn(x, lg, wgu, wd, sgu, sd, top_k=spec.k, alpha=spec.alpha, limit=spec.limit,
+                            interleaved=interleaved)
+        torch.cuda.synchronize()
+        assert torch.equal(again.out.view(torch.int16), res.out.view(torch.int16)), "second step differs"
     f8 = spec.w_dtype == "e4m3"
     ref = ref_moe(bf16_decode(act["x"]), act["logits"].astype(np.float64), _weights64(spec, w), spec.k,
                   storage="e4m3" if f8 else "bf16", act_quant=f8, alpha=spec.alpha, limit=spec.limit,
@@ -140,7 +148,7 @@ def test_moe_full_geometry_decode(name):
 
 @pytest.mark.parametrize("name", ["moe_prefill_bf16", "moe_prefill_e4m3"])
 def test_moe_full_geometry_prefill(name):
-    run_moe(MOE_SPECS[name])
+    run_moe(MOE_SPECS[name], repeat=True)
 
 
 def test_quantize_rows_e4m3_bit_exact():
