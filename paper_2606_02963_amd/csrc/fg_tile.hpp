@@ -143,25 +143,38 @@ __device__ __forceinline__ i32x4 make_buffer_rsrc(const void* base, uint32_t byt
                static_cast<int>(bytes), 0x00020000};
 }
 
-// Strided rows (dense x and W tiles): row r of the tile is at base + r·stride.
-// The descriptor covers the tile's valid rows only, so rows past the matrix
-// edge load as zeros. Every offset stays below 2^31 (the plan bounds
-// BM·stride), and each lane keeps one 32-bit offset instead of NLD pointers.
+// Strided rows (dense x and W tiles, MoE weight rows): the rows a lane loads
+// lie at a fixed byte step (pstride) from its first one (rowoff0) inside one
+// buffer descriptor, so each lane keeps one 32-bit offset instead of NLD
+// pointers. Offsets at or beyond the descriptor's size read as zero, which
+// is how rows past the matrix edge are filled. Every offset stays below
+// 2^31 (the plans bound the tile's byte span).
 template <int NLD, int RSTRIDE>
 struct BufRows {
   i32x4 rsrc;         // wave-uniform
-  uint32_t voff;      // (t >> 3)·stride + 16·(fetched chunk)
-  uint32_t pstride;   // RSTRIDE·stride
-  uint32_t stride;
+  uint32_t voff;      // rowoff0 + 16·(fetched chunk)
+  uint32_t pstride;   // bytes between a lane's successive rows
+  uint32_t rowoff0;   // byte offset of a lane's first row
 
+  // Tile rows r = (t >> 3) + RSTRIDE·p of a matrix whose rows are
+  // row_stride bytes apart; rows at or past rows_valid read as zero.
   __device__ __forceinline__ void init(const char* base, int64_t rows_valid, int64_t rows_tile, int64_t row_stride) {
     const int64_t rows = rows_valid < rows_tile ? rows_valid : rows_tile;
-    rsrc = make_buffer_rsrc(base, static_cast<uint32_t>(rows * row_stride));
-    stride = static_cast<uint32_t>(row_stride);
-    pstride = static_cast<uint32_t>(RSTRIDE * row_stride);
+    init_rows(base, static_cast<uint32_t>(rows * row_stride), static_cast<uint32_t>(threadIdx.x >> 3) *
+              static_cast<uint32_t>(row_stride), static_cast<uint32_t>(RSTRIDE * row_stride));
+  }
+
+  // A lane's rows at byte offsets first + pstride·p from `base`; bytes
+  // at or past `bytes` read as zero. `base` and `bytes` must be uniform
+  // across the wave.
+  __device__ __forceinline__ void init_rows(const char* base, uint32_t bytes, uint32_t first, uint32_t step) {
+    const i32x4 r = make_buffer_rsrc(base, bytes);
+    rsrc = i32x4{__builtin_amdgcn_readfirstlane(r[0]), __builtin_amdgcn_readfirstlane(r[1]),
+                 __builtin_amdgcn_readfirstlane(r[2]), __builtin_amdgcn_readfirstlane(r[3])};
+    pstride = step;
+    rowoff0 = first;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    voff = static_cast<uint32_t>(threadIdx.x >> 3) * stride +
-           static_cast<uint32_t>(((lane & 7) ^ (lane >> 3) ^ (wave & 1)) * 16);
+    voff = first + static_cast<uint32_t>(((lane & 7) ^ (lane >> 3) ^ (wave & 1)) * 16);
   }
 
   template <int NWAVES>
@@ -183,7 +196,7 @@ struct BufRows {
     const int c = threadIdx.x & 7;
     const int r0 = threadIdx.x >> 3;
     const int64_t off = kbyte + c * 16;
-    const uint32_t rowoff = static_cast<uint32_t>(r0) * stride + static_cast<uint32_t>(off);
+    const uint32_t rowoff = rowoff0 + static_cast<uint32_t>(off);
     const bool in = off < kbytes;
     i32x4 v[NLD];
 #pragma unroll

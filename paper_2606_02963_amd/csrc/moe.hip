@@ -21,6 +21,7 @@
 #include <math.h>
 
 #include <atomic>
+#include <type_traits>
 
 #include "fg_host.hpp"
 #include "fg_moe.hpp"
@@ -467,18 +468,43 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
   const int64_t rowbytes = a.K * TL::ESIZE;
   const int tr = threadIdx.x >> 3;
 
-  RowSet<TL::A_LD> ra;
-  RowSet<TL::B_LD> rb;
+  // A rows: gate/up gathers token rows through the permutation (a pointer
+  // per row); down reads the expert's consecutive h rows. B rows: the
+  // expert's weight rows, through one buffer descriptor and one offset per
+  // lane (rows past the valid range read as zero; their columns are never
+  // stored).
+  using ARows = typename std::conditional<EPI == EPI_GATEUP, RowSet<TL::A_LD>,
+                                          BufRows<TL::A_LD, TL::RSTRIDE>>::type;
+  ARows ra;
+  if constexpr (EPI == EPI_GATEUP) {
 #pragma unroll
-  for (int p = 0; p < TL::A_LD; ++p) {
-    int r = r0 + tr + TL::RSTRIDE * p;
-    r = r < seg1 ? r : seg0;
-    const int64_t arow = EPI == EPI_GATEUP ? (int64_t)(a.perm[r] / a.k) : (int64_t)r;
-    ra.ptr[p] = a.A + arow * rowbytes;
+    for (int p = 0; p < TL::A_LD; ++p) {
+      int r = r0 + tr + TL::RSTRIDE * p;
+      r = r < seg1 ? r : seg0;
+      ra.ptr[p] = a.A + (int64_t)(a.perm[r] / a.k) * rowbytes;
+    }
+  } else {
+    ra.init(a.A + (int64_t)r0 * rowbytes, seg1 - r0, TL::BM, rowbytes);
   }
+  BufRows<TL::B_LD, TL::RSTRIDE> rb;
   const char* We = a.W + (int64_t)e * a.Nw * rowbytes;
-#pragma unroll
-  for (int p = 0; p < TL::B_LD; ++p) rb.ptr[p] = We + weight_row<TL, EPI>(a, tn, tr + TL::RSTRIDE * p) * rowbytes;
+  if constexpr (EPI == EPI_GATEUP) {
+    // Lane t loads tile rows ρ = (t >> 3) + RSTRIDE·p, which interleave
+    // 16-row blocks of gate and up rows (weight_row). With RSTRIDE = 32
+    // every row of a lane is a gate row (t >> 7 even) or an up row, those of
+    // one wave alike, and they are h columns c0 + (t >> 3 & 15) + 16p.
+    static_assert(TL::RSTRIDE == 32 && TL::BN / 2 == 16 * TL::B_LD, "gate/up B rows: 16 h columns per load");
+    const int up = (threadIdx.x >> 7) & 1;
+    const int64_t c0 = (int64_t)tn * (TL::BN / 2);
+    const int64_t cols = a.I - c0 < TL::BN / 2 ? a.I - c0 : TL::BN / 2;    // valid h columns
+    const int64_t step = a.interleaved ? 2 : 1;                              // rows per h column
+    const char* base = We + (a.interleaved ? 2 * c0 + up : up * a.I + c0) * rowbytes;
+    const uint32_t bytes = static_cast<uint32_t>(((cols - 1) * step + 1) * rowbytes);
+    rb.init_rows(base, bytes, static_cast<uint32_t>(step * (tr & 15) * rowbytes),
+                 static_cast<uint32_t>(step * 16 * rowbytes));
+  } else {
+    rb.init(We + (int64_t)tn * TL::BN * rowbytes, a.Nw - (int64_t)tn * TL::BN, TL::BN, rowbytes);
+  }
 
   // Epilogue factors, loaded before the K loop so that their dependent
   // loads (slot → token → scale) complete behind it: per accumulator row the
