@@ -9,8 +9,9 @@
 //   offsets, stable permutation, m-tile prefix   moe_place_kernel
 //   grouped gate/up GEMM + clamped SwiGLU        grouped_kernel<.., EPI_GATEUP>
 //   [e4m3 only] quantise h per row               quantize_rows_kernel
-//   grouped down GEMM × routing weight           grouped_kernel<.., EPI_DOWN>
-//   finalize: Σ_j over the k slots of a token     moe_finalize_kernel
+//   grouped down GEMM, fp32 slot outputs          grouped_kernel<.., EPI_DOWN>
+//   finalize: Σ_j w_j·y over the k slots of a     moe_finalize_kernel
+//     token, one rounding to bf16
 // The token gather is folded into the gate/up GEMM's A-row addresses, and
 // the scatter back to slot order into the down GEMM's store addresses, so no
 // permuted copy of the tokens or of the outputs is ever materialised.
@@ -360,7 +361,7 @@ struct GroupedArgs {
   const int32_t* perm;     // [S] slot ids in expert order
   const int32_t* offsets;  // [E + 1]
   const int32_t* tile_off; // [E + 1]
-  const float* topk_w;     // [S] routing weights by slot id
+  const float* topk_w;     // [S] routing weights by slot id (unused: the finalize applies them)
   char* out;               // gate/up: h [S, I] bf16 (expert order); down: y_slot [S, H] fp32 (slot order)
   int E, k;
   int tiles_n;             // n-tiles of the output
@@ -506,28 +507,23 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
     rb.init(We + (int64_t)tn * TL::BN * rowbytes, a.Nw - (int64_t)tn * TL::BN, TL::BN, rowbytes);
   }
 
-  // Epilogue factors, loaded before the K loop so that their dependent
-  // loads (slot → token → scale) complete behind it: per accumulator row the
-  // scale of its activation row (e4m3) and, for the down GEMM, the routing
-  // weight of its slot; per column the weight-row scale (e4m3).
-  float rs[TL::FM][4];
+  // e4m3 dequantisation factors (per accumulator row the scale of its
+  // activation row, per column the weight-row scale), loaded before the K
+  // loop so that their dependent loads (slot → token → scale) complete
+  // behind it. The routing weight is applied in the finalize.
+  float rs[TL::IN == In::E4M3 ? TL::FM : 1][4];
+  float ws[TL::IN == In::E4M3 ? TL::FN : 1];
+  if constexpr (TL::IN == In::E4M3) {
 #pragma unroll
-  for (int fm = 0; fm < TL::FM; ++fm)
+    for (int fm = 0; fm < TL::FM; ++fm)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      int r = r0 + acc_row<TL>(fm, i);
-      r = r < seg1 ? r : seg0;
-      float sc = 1.0f;
-      if constexpr (TL::IN == In::E4M3)
-        sc = EPI == EPI_GATEUP ? a.a_scale[a.perm[r] / a.k] : a.a_scale[r];
-      if constexpr (EPI == EPI_DOWN) sc *= a.topk_w[a.perm[r]];
-      rs[fm][i] = sc;
-    }
-  float ws[TL::FN];
+      for (int i = 0; i < 4; ++i) {
+        int r = r0 + acc_row<TL>(fm, i);
+        r = r < seg1 ? r : seg0;
+        rs[fm][i] = EPI == EPI_GATEUP ? a.a_scale[a.perm[r] / a.k] : a.a_scale[r];
+      }
 #pragma unroll
-  for (int fn = 0; fn < TL::FN; ++fn) {
-    ws[fn] = 1.0f;
-    if constexpr (TL::IN == In::E4M3)
+    for (int fn = 0; fn < TL::FN; ++fn)
       ws[fn] = a.w_scale[(int64_t)e * a.Nw + weight_row<TL, EPI>(a, tn, acc_col<TL>(fn))];
   }
 
@@ -535,12 +531,14 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
   gemm_mainloop<TL>(ra, rb, rowbytes, lds, acc);
 
   const int l = threadIdx.x & 63, wave = threadIdx.x >> 6, wn = wave % TL::WN;
+  if constexpr (TL::IN == In::E4M3) {
 #pragma unroll
-  for (int fm = 0; fm < TL::FM; ++fm)
+    for (int fm = 0; fm < TL::FM; ++fm)
 #pragma unroll
-    for (int fn = 0; fn < TL::FN; ++fn)
+      for (int fn = 0; fn < TL::FN; ++fn)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) acc[fm][fn][i] *= rs[fm][i] * ws[fn];
+        for (int i = 0; i < 4; ++i) acc[fm][fn][i] *= rs[fm][i] * ws[fn];
+  }
 
   if constexpr (EPI == EPI_GATEUP) {
     const float alpha = a.alpha, limit = a.limit;
@@ -568,8 +566,8 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
     const int64_t ldo = a.ldo;
     const int n0 = tn * TL::BN;
     const int ncols = (int)(a.Nw - n0 < TL::BN ? a.Nw - n0 : TL::BN);
-    // The weighted slot outputs stay fp32 until the finalize's single
-    // rounding of the token sum. They are stored straight from the
+    // The slot outputs stay fp32; the finalize weights and sums them and
+    // rounds once. They are stored straight from the
     // accumulators: for each accumulator row, 16 lanes write 64 contiguous
     // bytes, and the neighbouring fragments of the same row complete the
     // line in L2 (measured faster than staging the fp32 tile through LDS in
@@ -600,15 +598,17 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
 }
 
 // ---------------------------------------------------------------------------
-// finalize: out[t, :] = Σ_j y_slot[t·k + j, :], j ascending, fp32 sum, bf16 out
-// (paper §IV-A, the MoE finalize kernel of Table I). One thread per 8
-// consecutive columns of a token; its K slot loads are all issued before the
-// first add, so a launch costs one memory round trip whatever K is. The slot
-// rows are bf16 (the standalone Table I kernel) or fp32 (inside the MoE step,
-// where the down GEMM leaves them unrounded).
+// finalize: out[t, :] = Σ_j w_j·y_slot[t·k + j, :], j ascending, fp32 sum,
+// bf16 out (paper §IV-A, the MoE finalize kernel of Table I). One thread per
+// 8 consecutive columns of a token; its K slot loads are all issued before
+// the first add, so a launch costs one memory round trip whatever K is. The
+// slot rows are bf16 and already weighted (the standalone Table I kernel,
+// w_j = 1) or fp32 (inside the MoE step, where the down GEMM leaves them
+// unrounded and unweighted, and w_j is the slot's routing weight).
 
 template <int K, class Y>
-__global__ __launch_bounds__(256) void moe_finalize_kernel(const Y* y_slot, uint16_t* out, int T, int64_t H) {
+__global__ __launch_bounds__(256) void moe_finalize_kernel(const Y* y_slot, const float* slot_w, uint16_t* out,
+                                                           int T, int64_t H) {
   const int64_t cpt = H / 8;
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int64_t t = idx / cpt, c = idx % cpt;
@@ -632,10 +632,14 @@ __global__ __launch_bounds__(256) void moe_finalize_kernel(const Y* y_slot, uint
 #pragma unroll
       for (int h = 0; h < 2; ++h)
         v[j][h] = *reinterpret_cast<const f32x4*>(y_slot + ((t * K + j) * H + c * 8 + h * 4));
+    // the routing weights of the token's slots, when given
+    float wj[K];
+#pragma unroll
+    for (int j = 0; j < K; ++j) wj[j] = slot_w != nullptr ? slot_w[t * K + j] : 1.0f;
 #pragma unroll
     for (int j = 0; j < K; ++j)
 #pragma unroll
-      for (int q = 0; q < 8; ++q) acc[q] += v[j][q >> 2][q & 3];
+      for (int q = 0; q < 8; ++q) acc[q] += wj[j] * v[j][q >> 2][q & 3];
   }
   i32x4 o;
 #pragma unroll
@@ -644,22 +648,24 @@ __global__ __launch_bounds__(256) void moe_finalize_kernel(const Y* y_slot, uint
   *reinterpret_cast<i32x4*>(out + (t * H + c * 8)) = o;
 }
 
-// Enqueue the finalize for top_k = k (1 .. KMAX) over slot rows of type Y.
+// Enqueue the finalize for top_k = k (1 .. KMAX) over slot rows of type Y,
+// weighting slot p by w[p] when w is given (fp32 slot rows only).
 template <class Y>
-static hipError_t launch_finalize(const Y* y, void* out, int64_t T, int64_t H, int k, hipStream_t s) {
+static hipError_t launch_finalize(const Y* y, const float* w, void* out, int64_t T, int64_t H, int k,
+                                  hipStream_t s) {
   const int64_t threads = T * (H / 8);
   const dim3 grid((unsigned)((threads + 255) / 256)), block(256);
   uint16_t* o = static_cast<uint16_t*>(out);
   const int t = (int)T;
   switch (k) {
-    case 1: return launch(moe_finalize_kernel<1, Y>, grid, block, 0, s, y, o, t, H);
-    case 2: return launch(moe_finalize_kernel<2, Y>, grid, block, 0, s, y, o, t, H);
-    case 3: return launch(moe_finalize_kernel<3, Y>, grid, block, 0, s, y, o, t, H);
-    case 4: return launch(moe_finalize_kernel<4, Y>, grid, block, 0, s, y, o, t, H);
-    case 5: return launch(moe_finalize_kernel<5, Y>, grid, block, 0, s, y, o, t, H);
-    case 6: return launch(moe_finalize_kernel<6, Y>, grid, block, 0, s, y, o, t, H);
-    case 7: return launch(moe_finalize_kernel<7, Y>, grid, block, 0, s, y, o, t, H);
-    default: return launch(moe_finalize_kernel<8, Y>, grid, block, 0, s, y, o, t, H);
+    case 1: return launch(moe_finalize_kernel<1, Y>, grid, block, 0, s, y, w, o, t, H);
+    case 2: return launch(moe_finalize_kernel<2, Y>, grid, block, 0, s, y, w, o, t, H);
+    case 3: return launch(moe_finalize_kernel<3, Y>, grid, block, 0, s, y, w, o, t, H);
+    case 4: return launch(moe_finalize_kernel<4, Y>, grid, block, 0, s, y, w, o, t, H);
+    case 5: return launch(moe_finalize_kernel<5, Y>, grid, block, 0, s, y, w, o, t, H);
+    case 6: return launch(moe_finalize_kernel<6, Y>, grid, block, 0, s, y, w, o, t, H);
+    case 7: return launch(moe_finalize_kernel<7, Y>, grid, block, 0, s, y, w, o, t, H);
+    default: return launch(moe_finalize_kernel<8, Y>, grid, block, 0, s, y, w, o, t, H);
   }
 }
 static_assert(KMAX == 8, "launch_finalize instantiates top_k 1 .. 8");
@@ -925,7 +931,7 @@ fg_status fg::moe_run(const char* fn, const moe_desc* d, const void* tokens, con
   else
     lc.add(big ? launch_grouped<GBf16Big, EPI_DOWN>(g, S, s) : launch_grouped<GBf16Small, EPI_DOWN>(g, S, s));
 
-  lc.add(launch_finalize(reinterpret_cast<const float*>(ws + L.y), out, d->T, d->H, d->top_k, s));
+  lc.add(launch_finalize(reinterpret_cast<const float*>(ws + L.y), topk_w, out, d->T, d->H, d->top_k, s));
   return check_launch(fn, lc);
 }
 
@@ -950,6 +956,7 @@ extern "C" fg_status moe_finalize(const void* y_slot, void* out, int64_t T, int6
   if (y_slot == nullptr || out == nullptr) return fail(FG_ERR_INVALID_ARG, "%s: NULL pointer", fn);
   if (!aligned16(y_slot) || !aligned16(out)) return fail(FG_ERR_ALIGNMENT, "%s: pointers must be 16-byte aligned", fn);
   Launches lc;
-  lc.add(launch_finalize(static_cast<const uint16_t*>(y_slot), out, T, H, top_k, static_cast<hipStream_t>(stream)));
+  lc.add(launch_finalize(static_cast<const uint16_t*>(y_slot), nullptr, out, T, H, top_k,
+                         static_cast<hipStream_t>(stream)));
   return check_launch(fn, lc);
 }
