@@ -44,9 +44,14 @@ template <> struct InTraits<In::F32>  { static constexpr int EPC = 4,  ESIZE = 4
 template <> struct InTraits<In::BF16> { static constexpr int EPC = 8,  ESIZE = 2; };
 template <> struct InTraits<In::E4M3> { static constexpr int EPC = 16, ESIZE = 1; };
 
-template <In IN_, int BM_, int BN_, int WM_ = 2, int WN_ = 2>
+// PRIO_: raise the wave priority (s_setprio 1) over each substep's MFMA and
+// fragment-read cluster, so that with two workgroups per compute unit a wave
+// that has matrix work ready issues it ahead of the other workgroup's loads
+// and barrier waits.
+template <In IN_, int BM_, int BN_, int WM_ = 2, int WN_ = 2, bool PRIO_ = false>
 struct Tile {
   static constexpr In IN = IN_;
+  static constexpr bool PRIO = PRIO_;
   static constexpr int BM = BM_, BN = BN_;
   static constexpr int WM = WM_, WN = WN_, NWAVES = WM * WN, THREADS = 64 * NWAVES;
   static constexpr int RSTRIDE = THREADS / 8;          // rows between a thread's successive loads
@@ -295,7 +300,8 @@ __device__ __forceinline__ void interleave_reads_with_mfma() {
 // stage s − 1 — and issues the direct loads of stage s + 1 into the buffer
 // stage s − 1 used. Loads past the last stage repeat the last stage into
 // that free buffer, which is never read again: the loop body needs no branch.
-template <class TL, class LA, class LB>
+// A wave that is not LIVE only loads and synchronises.
+template <class TL, bool LIVE, class LA, class LB>
 __device__ __forceinline__ void pipelined_substep(int64_t j, int64_t KT, const LA& ra, const LB& rb,
                                                   char* lds, int wm, int wn, const Frag<TL>& Fc, Frag<TL>& Fn,
                                                   f32x4 (&acc)[TL::FM][TL::FN]) {
@@ -311,9 +317,66 @@ __device__ __forceinline__ void pipelined_substep(int64_t j, int64_t KT, const L
     ra.template stage<TL::NWAVES>(sl * TL::ROWB, dst);
     rb.template stage<TL::NWAVES>(sl * TL::ROWB, dst + TL::BM * TL::ROWB);
   }
-  read_frag<TL>(lds + (s & 1) * TL::STAGE_BYTES, wm, wn, h, Fn);
-  mma_frag<TL>(Fc, acc);
-  interleave_reads_with_mfma<TL>();
+  if constexpr (LIVE) {
+    if constexpr (TL::PRIO) __builtin_amdgcn_s_setprio(1);
+    read_frag<TL>(lds + (s & 1) * TL::STAGE_BYTES, wm, wn, h, Fn);
+    mma_frag<TL>(Fc, acc);
+    interleave_reads_with_mfma<TL>();
+    if constexpr (TL::PRIO) __builtin_amdgcn_s_setprio(0);
+  }
+}
+
+// The K loop after its first loads (see gemm_mainloop); LIVE = false runs
+// the same loads and barriers without fragment reads or MFMAs.
+template <class TL, bool LIVE, class LA, class LB>
+__device__ __forceinline__ void mainloop_stages(const LA& ra, const LB& rb, int64_t KT, char* lds, int wm, int wn,
+                                                f32x4 (&acc)[TL::FM][TL::FN]) {
+  constexpr int SUB = Frag<TL>::SUB;
+  Frag<TL> F0, F1;
+  if constexpr (SUB == 1 && TL::FM * TL::FN > 8) {
+    // large e4m3 tiles: one substep per stage and 32-byte fragments; a
+    // second fragment set would not fit beside two resident workgroups, so
+    // each wave reads and multiplies in turn and the other workgroup's waves
+    // fill the gaps. (Small e4m3 tiles take the pipelined loop below, with
+    // one stage per substep.)
+    for (int64_t kt = 0; kt < KT; ++kt) {
+      if constexpr (LIVE) {
+        read_frag<TL>(lds + (kt & 1) * TL::STAGE_BYTES, wm, wn, 0, F0);
+        mma_frag<TL>(F0, acc);
+      }
+      wait_vmem();
+      __syncthreads();
+      const int64_t sl = kt + 2 < KT ? kt + 2 : KT - 1;
+      char* dst = lds + (kt & 1) * TL::STAGE_BYTES;
+      ra.template stage<TL::NWAVES>(sl * TL::ROWB, dst);
+      rb.template stage<TL::NWAVES>(sl * TL::ROWB, dst + TL::BM * TL::ROWB);
+    }
+  } else {
+    if constexpr (LIVE) read_frag<TL>(lds, wm, wn, 0, F0);
+    const int64_t J = KT * SUB;               // substeps
+    int64_t j = 0;
+    for (; j + 2 < J; j += 2) {
+      pipelined_substep<TL, LIVE>(j, KT, ra, rb, lds, wm, wn, F0, F1, acc);
+      pipelined_substep<TL, LIVE>(j + 1, KT, ra, rb, lds, wm, wn, F1, F0, acc);
+    }
+    // the last one or two substeps: multiply F0 before reading the final
+    // substep into the same registers (one fragment set live, not two, beside
+    // the accumulators); if the final substep opens the last stage its loads
+    // were issued long ago, so only the barrier is needed
+    if constexpr (LIVE) mma_frag<TL>(F0, acc);
+    if (J - j == 2) {
+      const int64_t s = (j + 1) / SUB;
+      const int h = static_cast<int>((j + 1) % SUB);
+      if (h == 0) {
+        wait_vmem();
+        __syncthreads();
+      }
+      if constexpr (LIVE) {
+        read_frag<TL>(lds + (s & 1) * TL::STAGE_BYTES, wm, wn, h, F0);
+        mma_frag<TL>(F0, acc);
+      }
+    }
+  }
 }
 
 // The K loop: acc = Σ_k A[rows]·B[rows]ᵀ over kbytes bytes of each row.
@@ -322,20 +385,24 @@ __device__ __forceinline__ void pipelined_substep(int64_t j, int64_t KT, const L
 // stages then stream through the two LDS buffers with direct loads issued
 // two stages ahead of the MFMAs that consume them, while the fragments of
 // substep j + 1 are read during the MFMAs of substep j. Ends with a
-// barrier, so the caller may reuse the LDS immediately.
+// barrier, so the caller may reuse the LDS immediately. A wave whose A rows
+// all lie at or past `rows_valid` (a ragged last row tile; wave-uniform)
+// only takes part in the loads and barriers: it reads no fragments and
+// issues no MFMAs, which leaves its SIMD to the other waves; its
+// accumulators stay zero.
 template <class TL, class LA, class LB>
 __device__ __forceinline__ void gemm_mainloop(const LA& ra, const LB& rb,
                                               int64_t kbytes, char* lds,
-                                              f32x4 (&acc)[TL::FM][TL::FN]) {
+                                              f32x4 (&acc)[TL::FM][TL::FN], int rows_valid = TL::BM) {
   constexpr int SUB = Frag<TL>::SUB;
   const int wave = threadIdx.x >> 6;
   const int wm = wave / TL::WN, wn = wave % TL::WN;
+  const bool live = __builtin_amdgcn_readfirstlane(wm * TL::TM < rows_valid ? 1 : 0) != 0;
 #pragma unroll
   for (int fm = 0; fm < TL::FM; ++fm)
 #pragma unroll
     for (int fn = 0; fn < TL::FN; ++fn) acc[fm][fn] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  Frag<TL> F0, F1;
   const int64_t KT = kbytes / TL::ROWB;   // full stages
   if (KT > 0) {
     ra.template stage<TL::NWAVES>(0, lds);
@@ -348,10 +415,13 @@ __device__ __forceinline__ void gemm_mainloop(const LA& ra, const LB& rb,
     ra.template tail<TL::RSTRIDE>(KT * TL::ROWB, kbytes, sb);
     rb.template tail<TL::RSTRIDE>(KT * TL::ROWB, kbytes, sb + TL::BM * TL::ROWB);
     __syncthreads();
+    if (live) {
+      Frag<TL> F;
 #pragma unroll
-    for (int h = 0; h < SUB; ++h) {
-      read_frag<TL>(sb, wm, wn, h, F0);
-      mma_frag<TL>(F0, acc);
+      for (int h = 0; h < SUB; ++h) {
+        read_frag<TL>(sb, wm, wn, h, F);
+        mma_frag<TL>(F, acc);
+      }
     }
     __syncthreads();
   }
@@ -365,46 +435,10 @@ __device__ __forceinline__ void gemm_mainloop(const LA& ra, const LB& rb,
     wait_vmem();
   }
   __syncthreads();
-  if constexpr (SUB == 1 && TL::FM * TL::FN > 8) {
-    // large e4m3 tiles: one substep per stage and 32-byte fragments; a
-    // second fragment set would not fit beside two resident workgroups, so
-    // each wave reads and multiplies in turn and the other workgroup's waves
-    // fill the gaps. (Small e4m3 tiles take the pipelined loop below, with
-    // one stage per substep.)
-    for (int64_t kt = 0; kt < KT; ++kt) {
-      read_frag<TL>(lds + (kt & 1) * TL::STAGE_BYTES, wm, wn, 0, F0);
-      mma_frag<TL>(F0, acc);
-      wait_vmem();
-      __syncthreads();
-      const int64_t sl = kt + 2 < KT ? kt + 2 : KT - 1;
-      char* dst = lds + (kt & 1) * TL::STAGE_BYTES;
-      ra.template stage<TL::NWAVES>(sl * TL::ROWB, dst);
-      rb.template stage<TL::NWAVES>(sl * TL::ROWB, dst + TL::BM * TL::ROWB);
-    }
-  } else {
-    read_frag<TL>(lds, wm, wn, 0, F0);
-    const int64_t J = KT * SUB;               // substeps
-    int64_t j = 0;
-    for (; j + 2 < J; j += 2) {
-      pipelined_substep<TL>(j, KT, ra, rb, lds, wm, wn, F0, F1, acc);
-      pipelined_substep<TL>(j + 1, KT, ra, rb, lds, wm, wn, F1, F0, acc);
-    }
-    // the last one or two substeps: multiply F0 before reading the final
-    // substep into the same registers (one fragment set live, not two, beside
-    // the accumulators); if the final substep opens the last stage its loads
-    // were issued long ago, so only the barrier is needed
-    mma_frag<TL>(F0, acc);
-    if (J - j == 2) {
-      const int64_t s = (j + 1) / SUB;
-      const int h = static_cast<int>((j + 1) % SUB);
-      if (h == 0) {
-        wait_vmem();
-        __syncthreads();
-      }
-      read_frag<TL>(lds + (s & 1) * TL::STAGE_BYTES, wm, wn, h, F0);
-      mma_frag<TL>(F0, acc);
-    }
-  }
+  if (live)
+    mainloop_stages<TL, true>(ra, rb, KT, lds, wm, wn, acc);
+  else
+    mainloop_stages<TL, false>(ra, rb, KT, lds, wm, wn, acc);
   wait_vmem();
   __syncthreads();
 }

@@ -129,7 +129,7 @@ __global__ __launch_bounds__(TL::THREADS) void fgemm_kernel(DenseArgs a, EpiArgs
   }
 
   f32x4 acc[TL::FM][TL::FN];
-  gemm_mainloop<TL>(ra, rb, kbytes, lds, acc);
+  gemm_mainloop<TL>(ra, rb, kbytes, lds, acc, a.M - m0 < TL::BM ? a.M - m0 : TL::BM);
   if (a.ks > 1 && !split_k_gather<TL>(a, tile, ks, acc, reinterpret_cast<unsigned*>(lds))) return;
 
   if constexpr (TL::IN == In::E4M3) {

@@ -490,19 +490,23 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
   BufRows<TL::B_LD, TL::RSTRIDE> rb;
   const char* We = a.W + (int64_t)e * a.Nw * rowbytes;
   if constexpr (EPI == EPI_GATEUP) {
-    // Lane t loads tile rows ρ = (t >> 3) + RSTRIDE·p, which interleave
-    // 16-row blocks of gate and up rows (weight_row). With RSTRIDE = 32
-    // every row of a lane is a gate row (t >> 7 even) or an up row, those of
-    // one wave alike, and they are h columns c0 + (t >> 3 & 15) + 16p.
-    static_assert(TL::RSTRIDE == 32 && TL::BN / 2 == 16 * TL::B_LD, "gate/up B rows: 16 h columns per load");
-    const int up = (threadIdx.x >> 7) & 1;
+    // Thread t loads tile rows ρ = tr + RSTRIDE·p, which interleave 16-row
+    // blocks of gate and up rows (weight_row): ρ is an up row when bit 4 of
+    // ρ is set, and h column (ρ >> 5)·16 + (ρ & 15) of the tile. RSTRIDE is
+    // a multiple of 32, so all rows of a thread are gate rows or all are up
+    // rows (those of one wave alike: tr >> 4 = wave >> 1), RSTRIDE / 2 h
+    // columns apart.
+    static_assert(TL::RSTRIDE % 32 == 0 && TL::BN / 2 == (TL::RSTRIDE / 2) * TL::B_LD,
+                  "gate/up B rows: RSTRIDE / 2 h columns per load");
+    const int up = (tr >> 4) & 1;
+    const int64_t col = (tr >> 5) * 16 + (tr & 15);
     const int64_t c0 = (int64_t)tn * (TL::BN / 2);
     const int64_t cols = a.I - c0 < TL::BN / 2 ? a.I - c0 : TL::BN / 2;    // valid h columns
     const int64_t step = a.interleaved ? 2 : 1;                              // rows per h column
     const char* base = We + (a.interleaved ? 2 * c0 + up : up * a.I + c0) * rowbytes;
     const uint32_t bytes = static_cast<uint32_t>(((cols - 1) * step + 1) * rowbytes);
-    rb.init_rows(base, bytes, static_cast<uint32_t>(step * (tr & 15) * rowbytes),
-                 static_cast<uint32_t>(step * 16 * rowbytes));
+    rb.init_rows(base, bytes, static_cast<uint32_t>(step * col * rowbytes),
+                 static_cast<uint32_t>(step * (TL::RSTRIDE / 2) * rowbytes));
   } else {
     rb.init(We + (int64_t)tn * TL::BN * rowbytes, a.Nw - (int64_t)tn * TL::BN, TL::BN, rowbytes);
   }
@@ -528,7 +532,7 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
   }
 
   f32x4 acc[TL::FM][TL::FN];
-  gemm_mainloop<TL>(ra, rb, rowbytes, lds, acc);
+  gemm_mainloop<TL>(ra, rb, rowbytes, lds, acc, seg1 - r0);
 
   const int l = threadIdx.x & 63, wave = threadIdx.x >> 6, wn = wave % TL::WN;
   if constexpr (TL::IN == In::E4M3) {
@@ -685,13 +689,17 @@ __global__ __launch_bounds__(256) void fill_i32_kernel(int32_t* p, int n, int v)
 // 256-row tiles lose more to the ragged last m-tile per
 // expert (n_e ≈ 512 ± 22 slots), and 128 × 256 fits one workgroup per unit.
 // Measured on the T = 4096 step: bf16 980–983 µs vs 1088–1090 µs with
-// 128 × 128, e4m3 697 vs 710–713 µs.
+// 128 × 128, e4m3 697 vs 710–713 µs; with the present kernels 256 × 256
+// (8 waves, one workgroup per unit, waves of empty row halves idle) and
+// 256 × 192 tiles take 1012 and 1052 µs against 939 µs. The bf16 prefill
+// tile raises the wave priority over its MFMA clusters (927 vs 944 µs);
+// the dense tiles do not (the LSE shape lost 3 % with it).
 // Decode e4m3 tiles are 192 weight rows wide: a tile then streams
 // 192 × H bytes, closer to the bf16 tile's 128 × 2H, so the per-tile start-up
 // is amortised over more bytes, and 192 divides the gpt-oss geometry exactly
 // (2880 = 30 × 96 h columns, 15 × 192 down rows). Measured: 161.8–162.2 µs vs
 // 165.1 µs for 128-row tiles and 177 µs for 256 on the T = 64 step.
-typedef Tile<In::BF16, 128, 192> GBf16Big;
+typedef Tile<In::BF16, 128, 192, 2, 2, true> GBf16Big;
 typedef Tile<In::BF16, 32, 128> GBf16Small;
 typedef Tile<In::E4M3, 128, 192> GF8Big;
 typedef Tile<In::E4M3, 32, 192> GF8Small;
@@ -710,14 +718,15 @@ static size_t align_up(size_t v) { return (v + 255) & ~(size_t)255; }
 // streaming). The launch dispatches on the same predicate, and the m-tile
 // prefix is built with the chosen tile's BM.
 static bool use_big_tiles(int64_t S, int E) { return S > (int64_t)48 * E; }
-static int pick_bm(int64_t S, int E) { return use_big_tiles(S, E) ? GBf16Big::BM : GBf16Small::BM; }
-static_assert(GBf16Big::BM == GF8Big::BM && GBf16Small::BM == GF8Small::BM,
-              "bf16 and e4m3 tiles must share BM: one m-tile prefix serves both");
+static int pick_bm(int64_t S, int E, int32_t w) {
+  if (w == FG_E4M3) return use_big_tiles(S, E) ? GF8Big::BM : GF8Small::BM;
+  return use_big_tiles(S, E) ? GBf16Big::BM : GBf16Small::BM;
+}
 
 static MoeLayout layout(const moe_desc& d) {
   MoeLayout L;
   L.S = d.T * d.top_k;
-  L.BM = pick_bm(L.S, d.E);
+  L.BM = pick_bm(L.S, d.E, d.w_dtype);
   size_t o = 0;
   L.nblocks = (int)((d.T + ROUTE_TOKENS - 1) / ROUTE_TOKENS);
   L.tile_off = o;
