@@ -22,9 +22,9 @@
  *     (paper §IV-A: the MoE decode path and its "MoE finalize" kernel,
  *     Table I; §V: optimising the whole MoE-MLP block jointly): top-k routing
  *     over router logits, a stable token permutation by expert, the grouped
- *     gate/up GEMM with a clamped-SwiGLU epilogue, the grouped down GEMM with
- *     the routing weight applied in its epilogue, and the finalize sum back to
- *     token order.
+ *     gate/up GEMM with a clamped-SwiGLU epilogue, the grouped down GEMM
+ *     (unweighted fp32 outputs per routed slot, in token order), and the
+ *     finalize, which weights each slot by its routing weight and sums them.
  *
  * Conventions shared by every entry point
  *  - All tensors are row-major and dense. W follows the nn.Linear layout
@@ -220,7 +220,11 @@ size_t moe_workspace_bytes(const moe_desc *d);
  *                  slot counts; expert e owns perm[offsets[e] .. offsets[e+1]).
  *   workspace, ws_bytes  at least moe_workspace_bytes(d).
  * Nothing is copied back to the host: the per-expert counts stay on the
- * device and the grouped GEMMs read them there.
+ * device and the grouped GEMMs read them there. Arithmetic: fp32
+ * accumulation; h (the SwiGLU output) is stored as bf16 (and, with e4m3
+ * weights, quantised per row to e4m3); the per-slot down outputs stay fp32
+ * and out is rounded once to bf16 after the weighted sum over j in
+ * ascending order, so results are bit-identical from call to call.
  */
 fg_status moe_grouped_ffn(const moe_desc *d, const void *tokens,
                           const float *router_logits, const void *w_gateup,
@@ -258,7 +262,8 @@ size_t moe_noalloc_scratch_bytes(void);
 
 /*
  * moe_finalize — the MoE finalize step on its own (paper §IV-A, the "MoE
- * finalize" kernel of Table I; also the last launch of moe_grouped_ffn):
+ * finalize" kernel of Table I; moe_grouped_ffn's last launch is the same
+ * kernel reading fp32 unweighted slot outputs and applying the weights):
  *   out[t, :] = Σ_{j = 0 .. top_k−1} y_slot[t·top_k + j, :]
  * summed in fp32 in ascending j, rounded once to bf16 (nearest even).
  *   y_slot  [T·top_k, H] bf16, row t·top_k + j = token t's j-th routed slot,

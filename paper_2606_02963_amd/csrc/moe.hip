@@ -361,7 +361,6 @@ struct GroupedArgs {
   const int32_t* perm;     // [S] slot ids in expert order
   const int32_t* offsets;  // [E + 1]
   const int32_t* tile_off; // [E + 1]
-  const float* topk_w;     // [S] routing weights by slot id (unused: the finalize applies them)
   char* out;               // gate/up: h [S, I] bf16 (expert order); down: y_slot [S, H] fp32 (slot order)
   int E, k;
   int tiles_n;             // n-tiles of the output
@@ -896,7 +895,6 @@ fg_status fg::moe_run(const char* fn, const moe_desc* d, const void* tokens, con
   g.perm = perm;
   g.offsets = expert_offsets;
   g.tile_off = tile_off;
-  g.topk_w = topk_w;
   g.E = d->E;
   g.k = d->top_k;
   g.I = d->I;
@@ -919,7 +917,7 @@ fg_status fg::moe_run(const char* fn, const moe_desc* d, const void* tokens, con
   else
     lc.add(big ? launch_grouped<GBf16Big, EPI_GATEUP>(g, S, s) : launch_grouped<GBf16Small, EPI_GATEUP>(g, S, s));
 
-  // down: [S, I] × [H, I]ᵀ → y_slot [S, H] (× routing weight, scattered to slot order)
+  // down: [S, I] × [H, I]ᵀ → y_slot [S, H] fp32, scattered to slot order (unweighted)
   const char* hA = ws + L.h;
   float* sh = reinterpret_cast<float*>(ws + L.sh);
   if (f8) {
