@@ -382,9 +382,10 @@ __device__ __forceinline__ void mainloop_stages(const LA& ra, const LB& rb, int6
 // The K loop: acc = Σ_k A[rows]·B[rows]ᵀ over kbytes bytes of each row.
 // `lds` must hold TL::LOOP_LDS bytes. A partial last stage (kbytes not a
 // multiple of 128) is loaded first through the zero-filling path; the full
-// stages then stream through the two LDS buffers with direct loads issued
-// two stages ahead of the MFMAs that consume them, while the fragments of
-// substep j + 1 are read during the MFMAs of substep j. Ends with a
+// stages then stream through the two LDS buffers, each stage's direct loads
+// in flight while the stage before it is multiplied (the large e4m3 tiles
+// issue stage s + 2 into the buffer stage s has just been read from), and
+// the fragments of substep j + 1 are read during the MFMAs of substep j. Ends with a
 // barrier, so the caller may reuse the LDS immediately. A wave whose A rows
 // all lie at or past `rows_valid` (a ragged last row tile; wave-uniform)
 // only takes part in the loads and barriers: it reads no fragments and
