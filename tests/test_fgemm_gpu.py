@@ -70,17 +70,20 @@ SMALL = [
     C2.scaled(M=300, N=520, K=264),                   # 128×128 tiles, ragged, K tail
     C2.scaled(M=2000, N=4104, K=136),                 # 256×256 tiles, ragged, K tail
     C2.scaled(M=4000, N=4000, K=200),                 # 256×256 tiles filling the chip, ragged
+    C2.scaled(M=3900, N=4000, K=200),                 # last row tile of 60 rows: its lower waves idle
     C2.scaled(M=1000, N=2056, K=4104),                # split-K over 4 slices, ragged, K tail
     C2.scaled(M=512, N=1024, K=8192),                 # split-K over 4 slices, 8 tiles
     C3.scaled(M=300, N=1000, K=264),                  # LSE across 8 N tiles, ragged N
     C3.scaled(M=70, N=100, K=64),                     # LSE inside one partial tile
     C3.scaled(M=2048, N=4096, K=128),                 # LSE with 256×128 tiles
     C3.scaled(M=4000, N=4000, K=200),                 # LSE with 256×256 tiles, ragged N
+    C3.scaled(M=3900, N=4000, K=200),                 # LSE, last row tile of 60 rows (idle waves)
     C3.scaled(M=1000, N=2056, K=4104),                # LSE after a split-K gather
     C4.scaled(M=300, N=512, K=264),                   # GroupNorm, 4 groups of 128
     FgemmSpec("gn64_ragged", 133, 320, 72, "bf16", 1 / 64, (("silu",),), "groupnorm", 5, 1e-5),
     C4.scaled(M=2048, N=4096, K=128),                 # GroupNorm with 256×128 tiles
     C4.scaled(M=4000, N=4096, K=200),                 # GroupNorm with 256×256 tiles
+    C4.scaled(M=3900, N=4096, K=200),                 # GroupNorm, last row tile of 60 rows (idle waves)
     C4.scaled(M=1000, N=2048, K=4104),                # GroupNorm after a split-K gather
     FgemmSpec("f32_gn_lse_chain", 96, 256, 64, "f32", 0.2, (("gelu_tanh",), ("scale", 1.5)), "lse"),
     FgemmSpec("f32_gn", 96, 256, 64, "f32", 0.2, (("silu",),), "groupnorm", 2, 1e-5),
