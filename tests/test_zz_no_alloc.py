@@ -72,3 +72,38 @@ def test_noalloc_matches_workspace_entry_point(w_dtype, T1, T2):
     rep = compare(host64(got[0]), ref["out"], "e4m3" if f8 else "bf16", slack=ref["out_bound"])
     log(f"    {rep}")
     assert rep.ok, rep
+
+
+def test_noalloc_graph_replays_match_eager():
+    """The callers this entry point is for include code under HIP graph
+    capture: a captured step, replayed with other calls on the same static
+    scratch in between, must reproduce the eager result bit for bit."""
+    require_gpu()
+    spec = MoeSpec("noalloc_graph", T=37, H=192, I=128, E=8, k=4)
+    other = MoeSpec("noalloc_graph_other", T=21, H=192, I=128, E=8, k=4)
+    w = make_moe_weights(spec, 41)
+    wgu, wd = dev_bf16(w["w_gate_up"]), dev_bf16(w["w_down"])
+    act, act2 = make_moe_activations(spec, 42), make_moe_activations(other, 43)
+    x, lg = dev_bf16(act["x"]), dev_f32(act["logits"])
+    x2, lg2 = dev_bf16(act2["x"]), dev_f32(act2["logits"])
+    desc = L.moe_desc(spec.T, spec.H, spec.I, spec.E, spec.k, "bf16")
+    desc2 = L.moe_desc(other.T, other.H, other.I, other.E, other.k, "bf16")
+    eager = _noalloc(desc, x, lg, wgu, wd, None, None)           # also looks up the scratch address
+    eager2 = _noalloc(desc2, x2, lg2, wgu, wd, None, None)
+    torch.cuda.synchronize()
+    bufs = [torch.empty_like(t) for t in eager]
+    p = lambda t: t.data_ptr()  # noqa: E731
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        L.moe_grouped_ffn_noalloc(desc, p(x), p(lg), p(wgu), p(wd), None, None, *[p(b) for b in bufs],
+                                  torch.cuda.current_stream().cuda_stream)
+    for r in range(3):
+        for b in bufs:
+            b.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        for name, got, want in zip(("out", "topk_idx", "topk_w", "perm", "offsets"), bufs, eager):
+            assert torch.equal(got.view(torch.int8), want.view(torch.int8)), f"replay {r}: {name} differs"
+        between = _noalloc(desc2, x2, lg2, wgu, wd, None, None)   # another call on the same scratch
+        torch.cuda.synchronize()
+        assert torch.equal(between[0].view(torch.int16), eager2[0].view(torch.int16))
