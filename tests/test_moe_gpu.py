@@ -85,6 +85,12 @@ SMALL = [
     MoeSpec("clamps_hit", T=64, H=128, I=128, E=4, k=2, x_std=10.0, w_std=0.05),
     MoeSpec("dense_E1", T=100, H=128, I=64, E=1, k=1),
     MoeSpec("prefill_big", T=2048, H=512, I=256, E=8, k=4),             # cancellation across slots
+    # either side of the row-tile switch (128-row tiles once experts average
+    # more than 48 slots): T·k = 1532 keeps 32-row tiles, 1540 takes 128-row
+    # tiles whose rows are mostly past the expert's slots (idle waves)
+    MoeSpec("tile_switch_small", T=383, H=256, I=192, E=32, k=4),
+    MoeSpec("tile_switch_big", T=385, H=256, I=192, E=32, k=4),
+    MoeSpec("tile_switch_big_e4m3", T=385, H=256, I=192, E=32, k=4, w_dtype="e4m3"),
 ]
 
 
