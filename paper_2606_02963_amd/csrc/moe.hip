@@ -424,10 +424,11 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
   };
   // Two tile orders. Both read the tile count from the device-side m-tile
   // prefix, and every workgroup reaches the end of its loop.
-  //  * large (prefill) tiles, one tile per workgroup: the real tiles, in expert-major
-  //    order (expert, n-tile, m-tile), are cut into 8 contiguous ranges, and
-  //    range x goes to the workgroups b ≡ x (mod 8), which the dispatcher
-  //    places on XCD x, in order. An expert's weights are then streamed by
+  //  * large (prefill) tiles: the real tiles, in expert-major order
+  //    (expert, n-tile, m-tile), are cut into 8 contiguous ranges, and range
+  //    x goes to the workgroups b ≡ x (mod 8), which the dispatcher places
+  //    on XCD x, in order: entry (b >> 3) + t·(G / 8) in round t (one round
+  //    when the grid covers every entry). An expert's weights are then streamed by
   //    one XCD (two at a range boundary) rather than by all eight, and the
   //    workgroups an XCD holds at a time cover every m-tile of the current
   //    expert over a run of n-tiles: each weight tile is used by all the
@@ -440,13 +441,14 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
   //    weight tile is fetched into one L2 and reused there.
   constexpr bool XCD_SPLIT = TL::BM > 32;
   const int mtiles = pick(toff_end, a.E - 1);
-  const int ntiles = XCD_SPLIT ? 1 : mtiles * a.tiles_n_grid;
-  for (int t = XCD_SPLIT ? 0 : blockIdx.x; t < ntiles; t += gridDim.x) {
+  const int ntiles = XCD_SPLIT ? 0x7fffffff : mtiles * a.tiles_n_grid;
+  for (int t = XCD_SPLIT ? 0 : blockIdx.x; t < ntiles; t += XCD_SPLIT ? 1 : gridDim.x) {
   int e = 0, mt, tn;
   if constexpr (XCD_SPLIT) {
+    // round t: workgroup b takes entry (b >> 3) + t·(G / 8) of range b mod 8
     const int total = mtiles * a.tiles_n;
     const int per = (total + 7) >> 3;
-    const int l = blockIdx.x >> 3;
+    const int l = (blockIdx.x >> 3) + t * (gridDim.x >> 3);
     const int u = (blockIdx.x & 7) * per + l;
     if (l >= per || u >= total) break;
 #pragma unroll
@@ -815,8 +817,16 @@ static hipError_t launch_grouped(GroupedArgs a, int64_t S, hipStream_t s) {
     grid = res < upper ? res : upper;
     grid = grid / 8 * 8 > 0 ? grid / 8 * 8 : 8;
   } else {
-    // 8 ranges of at most ceil(real tiles / 8) workgroups each
+    // 8 ranges of at most ceil(real tiles / 8) entries each. bf16 tiles take
+    // one entry per workgroup; e4m3 tiles run as many workgroups as are
+    // resident (a multiple of 8), each taking every (G / 8)-th entry of its
+    // range, so the m-tiles that share a weight tile start together in
+    // every round (e4m3 step 666.5 vs 679.3 µs; bf16 937 vs 921 µs).
     grid = 8 * ((mtiles * a.tiles_n + 7) / 8);
+    if constexpr (TL::IN == In::E4M3) {
+      const int64_t res = resident_workgroups<TL, EPI>() / 8 * 8;
+      if (res >= 8 && res < grid) grid = res;
+    }
   }
   return launch(grouped_kernel<TL, EPI>, dim3((unsigned)grid), dim3(TL::THREADS), 0, s, a);
 }
