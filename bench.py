@@ -468,8 +468,8 @@ def cpu_oracle_fgemm(spec, inp, budget_s, out, np):
 
 def grouped_epi(kernel_name):
     """0 for the gate/up grouped GEMM, 1 for the down GEMM, None otherwise."""
-    m = re.search(r"grouped_kernel<.*,\s*([01])>\(", kernel_name) or \
-        re.search(r"grouped_kernel.*Li([01])EEEvNS_11GroupedArgsE", kernel_name)
+    m = re.search(r"grouped_kernel<fg::Tile<[^>]*>,\s*([01])(?:,\s*(?:true|false))?>\(", kernel_name) or \
+        re.search(r"grouped_kernel.*Li([01])E(?:Lb[01]E)?EEvNS_11GroupedArgsE", kernel_name)
     return int(m.group(1)) if m else None
 
 

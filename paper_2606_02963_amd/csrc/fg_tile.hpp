@@ -85,8 +85,10 @@ __device__ __forceinline__ int lds_off(int row, int chunk) {
 // is even, so b & 1 = wave & 1 for every p.
 
 // Gathered rows (MoE token rows through the permutation): one pointer per
-// owned row. Rows past the matrix edge point at any valid row: their LDS copy
-// only feeds accumulator rows / columns that are never stored.
+// owned row, for matrices of more than 2^31 bytes (the MoE kernels gather
+// smaller ones through a buffer descriptor). Rows past the matrix edge point
+// at any valid row: their LDS copy only feeds accumulator rows / columns
+// that are never stored.
 template <int NLD>
 struct RowSet {
   const char* ptr[NLD];

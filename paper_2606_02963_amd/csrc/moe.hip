@@ -371,6 +371,58 @@ struct GroupedArgs {
   int64_t ldo;             // output row length in elements
   float alpha, limit;
   int interleaved;
+  uint32_t a_bytes;        // gate/up: bytes of the token matrix when at most 2^31
+};
+
+// Gathered rows of a matrix of at most 2^31 bytes: one buffer descriptor
+// over the whole matrix and a 32-bit byte offset per owned row, so the
+// stage loads are MUBUF loads with the LDS bit, like the strided rows (BufRows).
+// (With the global-segment form of the direct load in the loop, the
+// compiler waited for every LDS fragment read of a stage before its first
+// MFMA; with MUBUF loads it waits for each MFMA's own operands.) Rows past
+// the matrix edge take the offset of any valid row, as in RowSet.
+template <int NLD>
+struct GatherRows {
+  i32x4 rsrc;          // wave-uniform
+  uint32_t row[NLD];   // byte offset of each owned row
+  uint32_t cst;        // byte offset of the fetched chunk (see above)
+
+  // `base` and `bytes` (≤ 2^31) must be uniform across the wave.
+  __device__ __forceinline__ void init(const char* base, uint32_t bytes) {
+    const i32x4 r = make_buffer_rsrc(base, bytes);
+    rsrc = i32x4{__builtin_amdgcn_readfirstlane(r[0]), __builtin_amdgcn_readfirstlane(r[1]),
+                 __builtin_amdgcn_readfirstlane(r[2]), __builtin_amdgcn_readfirstlane(r[3])};
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    cst = static_cast<uint32_t>(((lane & 7) ^ (lane >> 3) ^ (wave & 1)) * 16);
+  }
+
+  template <int NWAVES>
+  __device__ __forceinline__ void stage(int64_t kbyte, char* sbase) const {
+    static_assert(NWAVES % 2 == 0, "the fetched chunk assumes an even wave count");
+    const int wave = threadIdx.x >> 6;
+#pragma unroll
+    for (int p = 0; p < NLD; ++p) {
+      char* dst = sbase + (wave + NWAVES * p) * 1024;
+      fg_raw_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(dst), 16,
+                             row[p] + cst + static_cast<uint32_t>(kbyte), 0, 0, 0);
+    }
+  }
+
+  // Every load is issued before the first LDS write (one memory round trip);
+  // chunks past kbytes get an out-of-range offset and read as zero.
+  template <int RS>
+  __device__ __forceinline__ void tail(int64_t kbyte, int64_t kbytes, char* sbase) const {
+    const int c = threadIdx.x & 7;
+    const int r0 = threadIdx.x >> 3;
+    const int64_t off = kbyte + c * 16;
+    const bool in = off < kbytes;
+    i32x4 v[NLD];
+#pragma unroll
+    for (int p = 0; p < NLD; ++p)
+      v[p] = fg_raw_buffer_load_b128(rsrc, in ? row[p] + static_cast<uint32_t>(off) : 0x80000000u, 0, 0);
+#pragma unroll
+    for (int p = 0; p < NLD; ++p) *reinterpret_cast<i32x4*>(sbase + lds_off(r0 + RS * p, c)) = v[p];
+  }
 };
 
 // LDS of a grouped workgroup: the main loop's two stages, or the bf16 h
@@ -401,7 +453,10 @@ __device__ __forceinline__ int64_t weight_row(const GroupedArgs& a, int tn, int 
   }
 }
 
-template <class TL, int EPI>
+// WIDE: the gate/up token matrix exceeds 2^31 bytes, so its gathered rows
+// are addressed by 64-bit pointers (RowSet) instead of 32-bit offsets into
+// one buffer descriptor (GatherRows).
+template <class TL, int EPI, bool WIDE>
 __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))) void grouped_kernel(GroupedArgs a) {
   __shared__ __attribute__((aligned(16))) char lds[GroupedLds<TL>::BYTES];
   // The m-tile prefix and the expert offsets, read once per workgroup into
@@ -475,15 +530,20 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
   // expert's weight rows, through one buffer descriptor and one offset per
   // lane (rows past the valid range read as zero; their columns are never
   // stored).
-  using ARows = typename std::conditional<EPI == EPI_GATEUP, RowSet<TL::A_LD>,
-                                          BufRows<TL::A_LD, TL::RSTRIDE>>::type;
+  using GRows = typename std::conditional<WIDE, RowSet<TL::A_LD>, GatherRows<TL::A_LD>>::type;
+  using ARows = typename std::conditional<EPI == EPI_GATEUP, GRows, BufRows<TL::A_LD, TL::RSTRIDE>>::type;
   ARows ra;
   if constexpr (EPI == EPI_GATEUP) {
+    if constexpr (!WIDE) ra.init(a.A, a.a_bytes);
 #pragma unroll
     for (int p = 0; p < TL::A_LD; ++p) {
       int r = r0 + tr + TL::RSTRIDE * p;
       r = r < seg1 ? r : seg0;
-      ra.ptr[p] = a.A + (int64_t)(a.perm[r] / a.k) * rowbytes;
+      const int64_t tok = a.perm[r] / a.k;
+      if constexpr (WIDE)
+        ra.ptr[p] = a.A + tok * rowbytes;
+      else
+        ra.row[p] = static_cast<uint32_t>(tok * rowbytes);
     }
   } else {
     ra.init(a.A + (int64_t)r0 * rowbytes, seg1 - r0, TL::BM, rowbytes);
@@ -786,7 +846,8 @@ static int resident_workgroups() {
   int v = cached[dev].load(std::memory_order_relaxed);
   if (v == 0) {
     int per_cu = 0, cus = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, grouped_kernel<TL, EPI>, TL::THREADS, 0) != hipSuccess ||
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, grouped_kernel<TL, EPI, false>, TL::THREADS, 0) !=
+            hipSuccess ||
         per_cu < 1)
       per_cu = 1;
     if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus < 1) cus = 256;
@@ -828,7 +889,14 @@ static hipError_t launch_grouped(GroupedArgs a, int64_t S, hipStream_t s) {
       if (res >= 8 && res < grid) grid = res;
     }
   }
-  return launch(grouped_kernel<TL, EPI>, dim3((unsigned)grid), dim3(TL::THREADS), 0, s, a);
+  if constexpr (EPI == EPI_GATEUP) {
+    // the token matrix: S / k rows of K elements
+    const int64_t a_bytes = S / a.k * a.K * TL::ESIZE;
+    if (a_bytes > ((int64_t)1 << 31))
+      return launch(grouped_kernel<TL, EPI, true>, dim3((unsigned)grid), dim3(TL::THREADS), 0, s, a);
+    a.a_bytes = static_cast<uint32_t>(a_bytes);
+  }
+  return launch(grouped_kernel<TL, EPI, false>, dim3((unsigned)grid), dim3(TL::THREADS), 0, s, a);
 }
 
 }  // namespace fg
@@ -901,7 +969,7 @@ fg_status fg::moe_run(const char* fn, const moe_desc* d, const void* tokens, con
                   (int)S, d->E, d->top_k, L.nblocks, L.BM, expert_offsets, tile_off, perm));
   }
 
-  GroupedArgs g;
+  GroupedArgs g{};
   g.perm = perm;
   g.offsets = expert_offsets;
   g.tile_off = tile_off;

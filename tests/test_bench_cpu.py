@@ -75,6 +75,11 @@ def test_grouped_gemm_work_per_launch():
     ("void fg::grouped_kernel<fg::Tile<(fg::In)1, 128, 192, 2, 2, true>, 0>(fg::GroupedArgs)", 0),
     ("void fg::grouped_kernel<fg::Tile<(fg::In)2, 128, 192, 2, 2, false>, 1>(fg::GroupedArgs)", 1),
     ("_ZN2fg14grouped_kernelINS_4TileILNS_2InE1ELi32ELi128ELi2ELi2ELb0EEELi1EEEvNS_11GroupedArgsE", 1),
+    ("void fg::grouped_kernel<fg::Tile<(fg::In)1, 128, 192, 2, 2, true>, 0, false>(fg::GroupedArgs)", 0),
+    ("void fg::grouped_kernel<fg::Tile<(fg::In)2, 128, 192, 2, 2, false>, 1, false>(fg::GroupedArgs)", 1),
+    ("void fg::grouped_kernel<fg::Tile<(fg::In)2, 32, 192, 2, 2, false>, 0, true>(fg::GroupedArgs)", 0),
+    ("_ZN2fg14grouped_kernelINS_4TileILNS_2InE1ELi32ELi128ELi2ELi2ELb0EEELi0ELb1EEEvNS_11GroupedArgsE", 0),
+    ("_ZN2fg14grouped_kernelINS_4TileILNS_2InE2ELi128ELi192ELi2ELi2ELb0EEELi1ELb0EEEvNS_11GroupedArgsE", 1),
     ("void fg::moe_finalize_kernel<4, float>(float const*, float const*, unsigned short*, int, long)", None),
 ])
 def test_grouped_kernel_names_parse(name, epi):

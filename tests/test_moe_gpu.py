@@ -249,31 +249,29 @@ def test_moe_validation_errors():
     assert ei.value.status == L.FG_ERR_WORKSPACE
 
 
-def test_moe_slots_past_4_gib():
-    """Maximum sizes: 190 000 tokens at top-4 give h and y_slot of more than
-    2^32 bytes (760 000 slot rows of 2880 bf16), so slot-row offsets past 32
-    bits are exercised in both grouped GEMMs and the finalize. Tokens and
-    logits repeat a seeded 64-token block on the device. Routing is checked
-    for every token against the block's oracle routing, the permutation and
-    offsets by their definition (numpy's stable argsort of the expert ids and
-    the exclusive prefix of their counts), and the outputs of sampled tokens,
-    including tokens whose h or y_slot rows lie past 4 GiB, against the
-    oracle."""
+def _repeated_block_step(name, T, w_dtype, seed):
+    """One step over T tokens that repeat a seeded 64-token block on the
+    device (tokens and logits). Routing is checked for every token against
+    the block's oracle routing, the permutation and offsets by their
+    definition (numpy's stable argsort of the expert ids and the exclusive
+    prefix of their counts). Returns the step's result, the block's oracle
+    result and the spec."""
     require_gpu()
-    R, T = 64, 190_000
-    spec = MoeSpec("slots_past_4gib", R)
-    act, w = make_moe_activations(spec, 21), make_moe_weights(spec, 21)
+    R = 64
+    spec = MoeSpec(name, R, w_dtype=w_dtype)
+    act, w = make_moe_activations(spec, seed), make_moe_weights(spec, seed)
     reps = (T + R - 1) // R
     x = dev_bf16(act["x"]).repeat(reps, 1)[:T]
     lg = dev_f32(act["logits"]).repeat(reps, 1)[:T]
-    wgu, wd, _, _ = _dev_weights(spec, w)
-    log(f"[moe] slots past 4 GiB T={T} H={spec.H} I={spec.I} E={spec.E} k={spec.k}")
-    res = api.moe_ffn(x, lg, wgu, wd, None, None, top_k=spec.k, alpha=spec.alpha, limit=spec.limit)
+    wgu, wd, sgu, sd = _dev_weights(spec, w)
+    log(f"[moe] {name} T={T} H={spec.H} I={spec.I} E={spec.E} k={spec.k} {w_dtype}")
+    res = api.moe_ffn(x, lg, wgu, wd, sgu, sd, top_k=spec.k, alpha=spec.alpha, limit=spec.limit)
     torch.cuda.synchronize()
-    S = T * spec.k
-    assert S * spec.I * 2 > 2 ** 32 and S * spec.H * 2 > 2 ** 32
+    del x, lg
+    f8 = w_dtype == "e4m3"
     ref = ref_moe(bf16_decode(act["x"]), act["logits"].astype(np.float64), _weights64(spec, w), spec.k,
-                  storage="bf16", act_quant=False, alpha=spec.alpha, limit=spec.limit, with_bound=True)
+                  storage="e4m3" if f8 else "bf16", act_quant=f8, alpha=spec.alpha, limit=spec.limit,
+                  with_bound=True)
     tok = np.arange(T) % R
     idx = res.topk_idx.cpu().numpy()
     assert np.array_equal(idx, ref["idx"][tok]), "top-k indices differ"
@@ -281,15 +279,53 @@ def test_moe_slots_past_4_gib():
     flat = idx.reshape(-1)
     counts = np.bincount(flat, minlength=spec.E)
     assert np.array_equal(res.offsets.cpu().numpy(), np.concatenate([[0], np.cumsum(counts)]))
+    assert np.array_equal(res.perm.cpu().numpy(), np.argsort(flat, kind="stable")), "permutation differs"
+    return res, ref, spec
+
+
+def _check_sampled_outputs(res, ref, spec, sample):
+    R = spec.T
+    got = host64(res.out[torch.from_numpy(sample).cuda()])
+    rep = compare(got, ref["out"][sample % R], spec.w_dtype, slack=ref["out_bound"][sample % R])
+    log(f"    {sample.size} sampled tokens: {rep}")
+    assert rep.ok, rep
+
+
+def test_moe_slots_past_4_gib():
+    """Maximum sizes: 190 000 tokens at top-4 give h and y_slot of more than
+    2^32 bytes (760 000 slot rows of 2880 bf16), so slot-row offsets past 32
+    bits are exercised in both grouped GEMMs and the finalize (the token
+    matrix itself, 1.09 GB, is gathered through 32-bit offsets). Outputs of
+    sampled tokens, including tokens whose h or y_slot rows lie past 4 GiB,
+    are checked against the oracle."""
+    T = 190_000
+    res, ref, spec = _repeated_block_step("slots_past_4gib", T, "bf16", 21)
+    S = T * spec.k
+    assert S * spec.I * 2 > 2 ** 32 and S * spec.H * 2 > 2 ** 32
     perm = res.perm.cpu().numpy()
-    assert np.array_equal(perm, np.argsort(flat, kind="stable")), "permutation differs"
     h_past = 2 ** 32 // (spec.I * 2)                     # first h row (expert order) needing 33 bits
     y_past = 2 ** 32 // (spec.H * 2)                     # first y_slot row (slot order) needing 33 bits
     h_late = np.unique(perm[h_past:] // spec.k)          # tokens with an h row past 4 GiB
     y_late = y_past // spec.k + 1                        # a token whose y_slot rows are all past 4 GiB
-    sample = np.unique(np.concatenate([[0, 1, R - 1, 100_000, y_late, T - 2, T - 1],
+    sample = np.unique(np.concatenate([[0, 1, spec.T - 1, 100_000, y_late, T - 2, T - 1],
                                        h_late[:: max(1, h_late.size // 6)]]))
-    got = host64(res.out[torch.from_numpy(sample).cuda()])
-    rep = compare(got, ref["out"][sample % R], "bf16", slack=ref["out_bound"][sample % R])
-    log(f"    {sample.size} sampled tokens: {rep}")
-    assert rep.ok, rep
+    _check_sampled_outputs(res, ref, spec, sample)
+
+
+@pytest.mark.parametrize("w_dtype", ["bf16", "e4m3"])
+def test_moe_tokens_past_2_gib(w_dtype):
+    """A token matrix of more than 2^31 bytes (800 000 tokens of 2880 values:
+    4.6 GB in bf16, 2.3 GB of e4m3 codes) is gathered by the gate/up GEMM
+    through 64-bit row addresses instead of 32-bit offsets; sampled tokens on
+    both sides of 2^31 (and, in bf16, of 2^32) bytes are checked against the
+    oracle."""
+    T = 800_000
+    res, ref, spec = _repeated_block_step(f"tokens_past_2gib_{w_dtype}", T, w_dtype, 22)
+    row = spec.H * (1 if w_dtype == "e4m3" else 2)       # bytes of one row of the gathered matrix
+    assert T * row > 2 ** 31
+    t2, t4 = 2 ** 31 // row, 2 ** 32 // row
+    sample = np.unique(np.concatenate([[0, 1, spec.T - 1, t2 - 1, t2, t2 + 1, T // 2, T - 2, T - 1],
+                                       [t4 - 1, t4, t4 + 1] if t4 < T else []]).astype(np.int64))
+    _check_sampled_outputs(res, ref, spec, sample)
+    del res
+    torch.cuda.empty_cache()
