@@ -870,8 +870,6 @@ static hipError_t launch_grouped(GroupedArgs a, int64_t S, hipStream_t s) {
   const int64_t upper = mtiles * a.tiles_n_grid;
   // Small (decode) tiles stream weights: size the grid to the resident
   // workgroups so that no partial last wave of workgroups idles the chip.
-  // Large (prefill) tiles keep one tile per workgroup, which measured ~5 %
-  // faster than the persistent loop there.
   int64_t grid;
   if (TL::BM <= 32) {
     const int64_t res = resident_workgroups<TL, EPI>();
