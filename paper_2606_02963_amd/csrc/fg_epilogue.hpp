@@ -67,9 +67,8 @@ __device__ __forceinline__ float apply_op_scalar(int kind, float a, float b, flo
 }
 
 // The chain runs over one block of FN·4 accumulators at a time (one fm),
-// all ops on that block before the next, so only that block is live in
-// VGPRs next to the transcendental temporaries; the accumulators stay in
-// AGPRs otherwise.
+// all ops on that block before the next, so only that block's temporaries
+// (the transcendental intermediates) are live beside the accumulators.
 template <class TL>
 __device__ __forceinline__ void apply_ops(const EpiArgs& ep, f32x4 (&acc)[TL::FM][TL::FN]) {
   if (ep.n_ops == 0) return;
