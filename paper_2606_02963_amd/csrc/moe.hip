@@ -465,13 +465,16 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
   // before it (a ballot), and its offsets come from lane shuffles, instead
   // of a chain of dependent global loads per tile.
   const int lane = threadIdx.x & 63;
-  int toff_end[4], off_beg[4];   // tile_off[i + 1] (INT_MAX past E), offsets[i] (i ≤ E)
+  int toff_end[4], off_beg[4];   // tile_off[i + 1] (INT_MAX past E), offsets[i] (i < E)
 #pragma unroll
   for (int q = 0; q < 4; ++q) {
     const int i = lane + 64 * q;
     toff_end[q] = i < a.E ? a.tile_off[i + 1] : 0x7fffffff;
-    off_beg[q] = i <= a.E ? a.offsets[i] : 0;
+    off_beg[q] = i < a.E ? a.offsets[i] : 0;
   }
+  // offsets[E], the end of the last expert's slots (entry 256 when E = 256
+  // would fall past the four registers)
+  const int off_end = a.offsets[a.E];
   auto pick = [&](const int (&v)[4], int i) {   // v[i / 64] of lane i mod 64 (i wave-uniform)
     const int q = i >> 6;
     const int x = q == 0 ? v[0] : q == 1 ? v[1] : q == 2 ? v[2] : v[3];
@@ -520,7 +523,7 @@ __global__ __launch_bounds__(TL::THREADS) __attribute__((amdgpu_waves_per_eu(2))
 #pragma unroll
     for (int q = 0; q < 4; ++q) e += __popcll(__ballot(toff_end[q] <= mt));
   }
-  const int seg0 = pick(off_beg, e), seg1 = pick(off_beg, e + 1);
+  const int seg0 = pick(off_beg, e), seg1 = e + 1 < a.E ? pick(off_beg, e + 1) : off_end;
   const int r0 = seg0 + (mt - (e == 0 ? 0 : pick(toff_end, e - 1))) * TL::BM;
   const int64_t rowbytes = a.K * TL::ESIZE;
   const int tr = threadIdx.x >> 3;

@@ -91,6 +91,17 @@ SMALL = [
     MoeSpec("tile_switch_small", T=383, H=256, I=192, E=32, k=4),
     MoeSpec("tile_switch_big", T=385, H=256, I=192, E=32, k=4),
     MoeSpec("tile_switch_big_e4m3", T=385, H=256, I=192, E=32, k=4, w_dtype="e4m3"),
+    # the largest expert count (256) and top-k (8): the grouped GEMMs' expert
+    # tables fill all four 64-entry lane registers and the last expert's end
+    # offset lies past them; routing rescans the logits in LDS on every pass
+    # (more than 32 experts); 32-row tiles, 128-row tiles in bf16 and e4m3,
+    # and a batch that leaves most experts empty; 129 experts end one entry
+    # into the third register
+    MoeSpec("experts_256_decode", T=200, H=128, I=64, E=256, k=8),
+    MoeSpec("experts_256_prefill", T=2048, H=128, I=64, E=256, k=8),
+    MoeSpec("experts_256_prefill_e4m3", T=2048, H=128, I=64, E=256, k=8, w_dtype="e4m3"),
+    MoeSpec("experts_256_sparse", T=16, H=128, I=64, E=256, k=8),
+    MoeSpec("experts_129", T=300, H=128, I=64, E=129, k=3),
 ]
 
 
