@@ -102,6 +102,9 @@ SMALL = [
     MoeSpec("experts_256_prefill_e4m3", T=2048, H=128, I=64, E=256, k=8, w_dtype="e4m3"),
     MoeSpec("experts_256_sparse", T=16, H=128, I=64, E=256, k=8),
     MoeSpec("experts_129", T=300, H=128, I=64, E=129, k=3),
+    # token rows (H) and h rows (I) longer than 4096 values: both e4m3
+    # quantisations take the two-pass path for long rows
+    MoeSpec("long_rows_e4m3", T=32, H=4160, I=4224, E=2, k=2, w_dtype="e4m3"),
 ]
 
 
@@ -166,6 +169,24 @@ def test_moe_full_geometry_decode(name):
 @pytest.mark.parametrize("name", ["moe_prefill_bf16", "moe_prefill_e4m3"])
 def test_moe_full_geometry_prefill(name):
     run_moe(MOE_SPECS[name], repeat=True)
+
+
+@pytest.mark.parametrize("cols", [4096, 4104, 12288])
+def test_quantize_rows_e4m3_long_rows(cols):
+    # 4096 values is the longest row quantised from registers in one pass;
+    # longer rows read the row twice (amax, then codes)
+    require_gpu()
+    rng = np.random.default_rng(cols)
+    rows = 9
+    x = rng.standard_normal((rows, cols)).astype(np.float32) * rng.random((rows, 1)).astype(np.float32) * 40
+    x[2] = 0.0
+    x[4, -1] = 1e4                                   # the row's maximum in its last chunk
+    bits = to_bf16_bits(x)
+    q, s = api.quantize_rows_e4m3(dev_bf16(bits))
+    torch.cuda.synchronize()
+    q_ref, s_ref = ref_quant_rows_e4m3(bf16_decode(bits))
+    assert np.array_equal(s.cpu().numpy().astype(np.float64), s_ref)
+    assert np.array_equal(q.cpu().numpy(), q_ref)
 
 
 def test_quantize_rows_e4m3_bit_exact():
