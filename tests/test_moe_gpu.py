@@ -40,7 +40,8 @@ def _dev_weights(spec, w):
             dev_f32(w["s_down"]))
 
 
-def run_moe(spec, seed=0, act=None, w=None, tokens=None, interleaved=False, check_out=True, repeat=False):
+def run_moe(spec, seed=0, act=None, w=None, tokens=None, interleaved=False, check_out=True, repeat=False,
+            oracle_logits=None):
     require_gpu()
     log(f"[moe] {spec.name} T={spec.T} H={spec.H} I={spec.I} E={spec.E} k={spec.k} {spec.w_dtype} seed={seed}")
     act = act if act is not None else make_moe_activations(spec, seed)
@@ -58,7 +59,8 @@ def run_moe(spec, seed=0, act=None, w=None, tokens=None, interleaved=False, chec
         torch.cuda.synchronize()
         assert torch.equal(again.out.view(torch.int16), res.out.view(torch.int16)), "second step differs"
     f8 = spec.w_dtype == "e4m3"
-    ref = ref_moe(bf16_decode(act["x"]), act["logits"].astype(np.float64), _weights64(spec, w), spec.k,
+    lg64 = (act["logits"] if oracle_logits is None else oracle_logits).astype(np.float64)
+    ref = ref_moe(bf16_decode(act["x"]), lg64, _weights64(spec, w), spec.k,
                   storage="e4m3" if f8 else "bf16", act_quant=f8, alpha=spec.alpha, limit=spec.limit,
                   interleaved=interleaved, tokens=tokens, with_bound=True)
     assert np.array_equal(res.topk_idx.cpu().numpy(), ref["idx"]), "top-k indices differ"
@@ -119,6 +121,27 @@ def test_moe_logit_ties_route_to_lower_index():
     act["logits"] = (np.round(act["logits"] * 2) / 2).astype(np.float32)   # many exact ties
     act["logits"][5, :] = 0.25                                              # a fully tied row
     run_moe(spec, act=act)
+
+
+def test_moe_nan_and_signed_zero_logits():
+    # a NaN logit ranks below every number (never chosen while k finite
+    # logits remain), and −0 ties with +0 (the lower index first); the
+    # oracle routes the same logits with each NaN written as −∞
+    spec = MoeSpec("nan_zero", T=70, H=128, I=64, E=32, k=4)
+    act = make_moe_activations(spec, 5)
+    lg = act["logits"]
+    lg[0, [3, 7, 11]] = np.nan
+    lg[1, :] = -5.0
+    lg[1, [2, 9]] = 0.0
+    lg[1, [5, 30]] = -0.0
+    lg[2, :28] = np.nan                                # exactly k finite logits left
+    lg[65, 0] = np.nan                                 # a token of the second 64-token block
+    run_moe(spec, act=act, oracle_logits=np.where(np.isnan(lg), -np.inf, lg))
+
+
+@pytest.mark.parametrize("k", [5, 6, 7])
+def test_moe_top_k_5_to_7(k):
+    run_moe(MoeSpec(f"top{k}", T=50, H=128, I=64, E=16, k=k))
 
 
 def test_moe_interleaved_gate_up():
@@ -236,7 +259,8 @@ def test_moe_finalize_table_i_batches(T):
     assert rep.ok, rep
 
 
-@pytest.mark.parametrize("T,H,k", [(3, 8, 1), (5, 24, 3), (2, 136, 8), (7, 2880, 2)])
+@pytest.mark.parametrize("T,H,k", [(3, 8, 1), (5, 24, 3), (2, 136, 8), (7, 2880, 2), (4, 64, 5), (3, 40, 6),
+                                   (6, 16, 7)])
 def test_moe_finalize_edge_shapes(T, H, k):
     """Minimum width (one 8-column chunk), odd T, k = 1 (a copy), k = 8 (the
     largest top_k), and widths that are not a multiple of the workgroup."""
