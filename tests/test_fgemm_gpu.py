@@ -172,6 +172,17 @@ TABLE3 += [
     FgemmSpec("f32_lse_mish", 96, 256, 64, "f32", 0.2, (("scale", 2.0),), "lse", post_ops=(("mish",),)),
     FgemmSpec("f32_gn_lrelu", 96, 256, 64, "f32", 0.2, (), "groupnorm", 2, 1e-5,
               post_ops=(("leaky_relu", 0.01), ("scale", 2.0))),
+    # the longest post chains (8 ops) after each reduction, the GroupNorm one
+    # also in the second launch (groups of 96 channels)
+    FgemmSpec("bf16_lse_post8", 130, 1000, 200, "bf16", 0.1, (("add", -0.25),), "lse",
+              post_ops=(("scale", 0.5), ("add", 0.1), ("mish",), ("leaky_relu", 0.1), ("silu",),
+                        ("gelu_tanh",), ("clamp", -1.0, 2.0), ("relu",))),
+    FgemmSpec("bf16_gn_post8", 130, 512, 200, "bf16", 0.1, (("silu",),), "groupnorm", 4, 1e-5,
+              post_ops=(("scale", 0.5), ("add", 0.1), ("mish",), ("leaky_relu", 0.1), ("silu",),
+                        ("gelu_tanh",), ("clamp", -1.0, 2.0), ("relu",))),
+    FgemmSpec("bf16_gn96_post8", 130, 576, 200, "bf16", 0.1, (("silu",),), "groupnorm", 6, 1e-5,
+              post_ops=(("scale", 0.5), ("add", 0.1), ("mish",), ("leaky_relu", 0.1), ("silu",),
+                        ("gelu_tanh",), ("clamp", -1.0, 2.0), ("relu",))),
 ]
 
 
