@@ -107,6 +107,12 @@ SMALL = [
     # token rows (H) and h rows (I) longer than 4096 values: both e4m3
     # quantisations take the two-pass path for long rows
     MoeSpec("long_rows_e4m3", T=32, H=4160, I=4224, E=2, k=2, w_dtype="e4m3"),
+    # the smallest H and I (64): in bf16 each contraction is one full stage,
+    # in e4m3 only a partial one (64 of a stage's 128 bytes, no full stage)
+    MoeSpec("min_dims", T=40, H=64, I=64, E=4, k=2),
+    MoeSpec("min_dims_e4m3", T=40, H=64, I=64, E=4, k=2, w_dtype="e4m3"),
+    MoeSpec("min_dims_big", T=200, H=64, I=64, E=4, k=2),
+    MoeSpec("min_dims_big_e4m3", T=200, H=64, I=64, E=4, k=2, w_dtype="e4m3"),
 ]
 
 
