@@ -65,6 +65,14 @@ def run_spec(spec, seed=0, rows=None, inp=None, with_bias=True):
 C1, C2, C3, C4 = (FGEMM_SPECS[k] for k in ("tiny_f32_relu_x2", "bf16_gelu_clamp", "bf16_lse", "bf16_silu_gn"))
 
 SMALL = [
+    # the smallest shapes each input type and reduction admits: one row, one
+    # 16-byte chunk of K (a partial stage only), one output chunk; LSE over
+    # a single column; one GroupNorm group of 8 channels (the second launch)
+    FgemmSpec("min_bf16", 1, 8, 8, "bf16", 0.1, (("gelu_tanh",),)),
+    FgemmSpec("min_f32", 1, 4, 4, "f32", 0.2, (("relu",),)),
+    FgemmSpec("min_e4m3", 1, 8, 16, "e4m3", 0.1, (("silu",),), out_dtype="bf16"),
+    FgemmSpec("min_lse_one_column", 3, 1, 8, "bf16", 0.1, (("add", -0.25),), "lse"),
+    FgemmSpec("min_gn_one_group", 2, 8, 8, "bf16", 0.1, (), "groupnorm", 1, 1e-5),
     C1,                                               # the fp32 workload at full size
     C1.scaled(M=77, N=200, K=36, name="f32_ragged"),  # K tail (36 % 32), ragged M, N
     C2.scaled(M=300, N=520, K=264),                   # 128×128 tiles, ragged, K tail
