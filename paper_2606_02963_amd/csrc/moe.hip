@@ -2,11 +2,12 @@
 //
 // Launch sequence on the caller's stream, with no host synchronisation (the
 // per-expert counts never leave the device):
-//   [e4m3 only] quantise tokens per row          quantize_rows_kernel
-//     (with one routing block: inside the routing launch)
 //   route: top-k + softmax per token, and the    moe_route_kernel
-//     expert histogram of each block of tokens
+//     expert histogram of each block of tokens;
+//     [e4m3 only] the tokens quantised per row
+//     by further blocks of the same launch
 //   offsets, stable permutation, m-tile prefix   moe_place_kernel
+//     (with one routing block: inside the routing launch)
 //   grouped gate/up GEMM + clamped SwiGLU        grouped_kernel<.., EPI_GATEUP>
 //   [e4m3 only] quantise h per row               quantize_rows_kernel
 //   grouped down GEMM, fp32 slot outputs          grouped_kernel<.., EPI_DOWN>
@@ -188,10 +189,12 @@ __global__ __launch_bounds__(64 * ROUTE_WAVES) void moe_route_kernel(const float
                                                                      int32_t* offsets, int32_t* tile_off,
                                                                      int32_t* perm, const uint16_t* xq_src,
                                                                      int64_t H, uint8_t* xq, float* sx) {
-  // Single-block routing may share its launch with the e4m3 quantisation of
-  // the tokens (independent work): blocks 1, 2, ... take four token rows each.
-  if (FUSED_PLACE && blockIdx.x > 0) {
-    quantize_row_wave(xq_src, T, H, xq, sx, (int64_t)(blockIdx.x - 1) * 4 + (threadIdx.x >> 6));
+  // Routing shares its launch with the e4m3 quantisation of the tokens
+  // (independent work): the blocks after the routing blocks take four token
+  // rows each.
+  const int rblocks = (T + ROUTE_TOKENS - 1) / ROUTE_TOKENS;
+  if ((int)blockIdx.x >= rblocks) {
+    quantize_row_wave(xq_src, T, H, xq, sx, (int64_t)(blockIdx.x - rblocks) * 4 + (threadIdx.x >> 6));
     return;
   }
   // row pitch E + 1 floats: thread t reading its row's logit e hits bank (t·(E+1) + e) mod 64
@@ -950,22 +953,19 @@ fg_status fg::moe_run(const char* fn, const moe_desc* d, const void* tokens, con
   float* sx = reinterpret_cast<float*>(ws + L.sx);
   uint8_t* xq = f8 ? reinterpret_cast<uint8_t*>(ws + L.xq) : nullptr;
   const uint16_t* tok16 = static_cast<const uint16_t*>(tokens);
-  if (f8) {
-    a_tokens = ws + L.xq;
-    if (L.nblocks > 1)
-      lc.add(launch(quantize_rows_kernel, dim3((unsigned)((d->T + 3) / 4)), dim3(256), 0, s, tok16, d->T, d->H, xq,
-                    sx));
-  }
+  if (f8) a_tokens = ws + L.xq;
   int32_t* counts = reinterpret_cast<int32_t*>(ws + L.counts);
+  // with e4m3 the token quantisation rides in the routing launch: four rows
+  // per block after the routing blocks
+  const unsigned qblocks = f8 ? (unsigned)((d->T + 3) / 4) : 0u;
   if (L.nblocks == 1) {
-    // one routing block; with e4m3 the token quantisation rides in the same launch
-    const unsigned qblocks = f8 ? (unsigned)((d->T + 3) / 4) : 0u;
+    // one routing block, which also places the slots
     lc.add(launch(moe_route_kernel<true>, dim3(1 + qblocks), dim3(64 * ROUTE_WAVES), 0, s, router_logits, T, d->E,
                   d->top_k, topk_idx, topk_w, counts, L.BM, expert_offsets, tile_off, perm, tok16, d->H, xq, sx));
   } else {
-    lc.add(launch(moe_route_kernel<false>, dim3((unsigned)L.nblocks), dim3(64 * ROUTE_WAVES), 0, s, router_logits, T,
-                  d->E, d->top_k, topk_idx, topk_w, counts, L.BM, expert_offsets, tile_off, perm, tok16, d->H, xq,
-                  sx));
+    lc.add(launch(moe_route_kernel<false>, dim3((unsigned)L.nblocks + qblocks), dim3(64 * ROUTE_WAVES), 0, s,
+                  router_logits, T, d->E, d->top_k, topk_idx, topk_w, counts, L.BM, expert_offsets, tile_off, perm,
+                  tok16, d->H, xq, sx));
     lc.add(launch(moe_place_kernel, dim3((unsigned)L.nblocks), dim3(64 * PLACE_WAVES), 0, s, topk_idx, counts,
                   (int)S, d->E, d->top_k, L.nblocks, L.BM, expert_offsets, tile_off, perm));
   }
