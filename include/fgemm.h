@@ -183,7 +183,8 @@ fg_status fgemm_plan_info(const fg_plan *plan, int32_t *tile_m, int32_t *tile_n,
 /* MoE expert FFN                                                         */
 
 typedef struct {
-  int64_t T;                /* tokens (0 allowed: nothing is enqueued) */
+  int64_t T;                /* tokens (0 allowed: only expert_offsets is
+                               written, all zeros) */
   int64_t H;                /* hidden size; multiple of 64 */
   int64_t I;                /* expert intermediate size; multiple of 64 */
   int32_t E;                /* experts, 1 .. 256 */
