@@ -114,7 +114,9 @@ typedef struct fg_plan fg_plan; /* opaque, host memory, immutable once built */
  *            K = 0 gives z = b. Each must be < 2^31.
  *   in_dtype FG_F32, FG_BF16 or FG_E4M3 for both x and W. K must be a
  *            multiple of 4 (f32), 8 (bf16) or 16 (e4m3) so that rows stay
- *            16-byte aligned (FG_ERR_ALIGNMENT otherwise). FG_E4M3 is the W8A8
+ *            16-byte aligned (FG_ERR_ALIGNMENT otherwise), and a row of x or
+ *            W may hold at most 4 MiB (K·element size; FG_ERR_UNSUPPORTED
+ *            beyond, since tile operands use 32-bit offsets). FG_E4M3 is the W8A8
  *            form: OCP e4m3fn codes with one fp32 scale per row of x and per
  *            row of W, run with fgemm_run_scaled; the fp8 MFMA accumulates in
  *            fp32 and z = (Σ_k qx·qw)·sx[m]·sw[n] + b before the tail.
