@@ -77,7 +77,10 @@ def ref_swiglu_clamped(gate, up, alpha=1.702, limit=7.0):
     """Clamped SwiGLU: (clip(up, −L, L) + 1) · g·σ(α·g), g = min(gate, L)."""
     g = np.minimum(gate, limit)
     u = np.clip(up, -limit, limit)
-    sig = 1.0 / (1.0 + np.exp(-alpha * g))
+    # for very negative α·g the exponential overflows to +inf and σ is 0,
+    # its exact limit; the overflow is expected, not an error
+    with np.errstate(over="ignore"):
+        sig = 1.0 / (1.0 + np.exp(-alpha * g))
     return (u + 1.0) * (g * sig)
 
 
