@@ -135,18 +135,32 @@ def store_h(h, storage):
 FRAGILE_REL = 2.0 ** -16
 FRAGILE_ABS = 2.0 ** -20
 
+# Accumulation noise of an e4m3 × e4m3 contraction on the matrix cores, as a
+# fraction of Σ|x_i·w_i| over the contraction. The 128-wide fp8 dot product
+# of gfx950's f8f6f4 MFMA is not summed as IEEE fp32: products far below the
+# largest one of the dot product lose low-order bits. Measured: at most
+# 2.4e-5 of Σ|products| on Gaussian data (150 000 dot products), up to
+# 2.6e-4 when one product dominates the other 127. For the W8A8 step the
+# neighbourhood of a storage boundary of h widens by this noise, carried
+# through the clamped SwiGLU; the value is 2.5× the Gaussian-data maximum
+# (the synthetic workloads are Gaussian), not a worst-case bound.
+F8_DOT_NOISE = 2.0 ** -14
 
-def storage_deviation(h, storage):
+
+def storage_deviation(h, storage, noise=None):
     """Largest change of the stored value of each element of h (per row for
     the per-row-scaled e4m3 storage) over the rounding decisions that are
-    within FRAGILE_REL·|h| + FRAGILE_ABS·max|h_row| of a boundary. Zero for
-    every element whose stored value is robust. Returns (stored, deviation),
-    stored being store_h(h, storage)."""
+    within FRAGILE_REL·|h| + FRAGILE_ABS·max|h_row| (+ noise, a per-element
+    absolute bound on how far a kernel's h may lie from the exact one) of a
+    boundary. Zero for every element whose stored value is robust. Returns
+    (stored, deviation), stored being store_h(h, storage)."""
     h = np.asarray(h, dtype=np.float64)
     stored = store_h(h, storage)
     if storage == "none":
         return stored, np.zeros_like(h)
     pert = FRAGILE_REL * np.abs(h) + FRAGILE_ABS * np.max(np.abs(h), axis=-1, keepdims=True)
+    if noise is not None:
+        pert = pert + np.asarray(noise, dtype=np.float64)
     b_ref, b_lo, b_hi = _bf16(h), _bf16(h - pert), _bf16(h + pert)
     if storage == "bf16":
         return stored, np.maximum(np.abs(b_lo - b_ref), np.abs(b_hi - b_ref))
@@ -170,6 +184,19 @@ def storage_deviation(h, storage):
         moved = e4m3_decode(e4m3_encode_rne_sat(f32_round(f32_round(b[r, c]) / sc))) * sc
         dev[r, c] = np.maximum(dev[r, c], np.abs(moved - stored[r, c]))
     return stored, dev
+
+
+def swiglu_noise(gate, up, d_gate, d_up, alpha=1.702, limit=7.0):
+    """Largest change of the clamped SwiGLU when gate and up move by at most
+    d_gate and d_up: the four corners of that box. The function is monotone
+    in the clamped up value and smooth in gate, so over intervals this small
+    its extremes lie at the corners."""
+    h0 = ref_swiglu_clamped(gate, up, alpha, limit)
+    n = np.zeros_like(h0)
+    for sg in (-1.0, 1.0):
+        for su in (-1.0, 1.0):
+            n = np.maximum(n, np.abs(ref_swiglu_clamped(gate + sg * d_gate, up + su * d_up, alpha, limit) - h0))
+    return n
 
 
 def _split_gate_up(G, I, interleaved):
@@ -211,7 +238,13 @@ def ref_expert_rows(X, W_gu, W_d, storage="bf16", act_quant=False, alpha=1.702,
     h = ref_swiglu_clamped(gate, up, alpha, limit)
     W_d = np.asarray(W_d, dtype=np.float64)
     if with_bound:
-        h, dev = storage_deviation(h, storage)
+        noise = None
+        if act_quant:
+            # the e4m3 contraction's accumulation noise, per element of G
+            dG = F8_DOT_NOISE * (np.abs(X) @ np.abs(np.asarray(W_gu, dtype=np.float64)).T)
+            d_gate, d_up = _split_gate_up(dG, I, interleaved)
+            noise = swiglu_noise(gate, up, d_gate, d_up, alpha, limit)
+        h, dev = storage_deviation(h, storage, noise)
         return h @ W_d.T, dev @ np.abs(W_d).T
     return store_h(h, storage) @ W_d.T
 
@@ -227,9 +260,10 @@ def ref_moe(x, logits, weights, k, storage="bf16", act_quant=False, alpha=1.702,
     output depends only on its own row and its own routing).
     with_bound: also return "out_bound", per output element the largest
     change any storage-rounding decision of h within the fragile
-    neighbourhood of a boundary (see storage_deviation) can cause; a kernel
-    that evaluates h in another rounding order may take those decisions
-    either way, and every such result is correct.
+    neighbourhood of a boundary (see storage_deviation; with act_quant it
+    includes the e4m3 contraction's accumulation noise, F8_DOT_NOISE) can
+    cause; a kernel that evaluates h in another rounding order may take
+    those decisions either way, and every such result is correct.
     Returns a dict: out [T or len(tokens), H], idx, w, counts, offsets, perm
     (and out_bound).
     """

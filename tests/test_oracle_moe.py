@@ -317,6 +317,43 @@ def test_storage_deviation_bound():
     assert FRAGILE_REL < 1e-4
 
 
+def test_storage_deviation_noise_and_swiglu_noise(monkeypatch):
+    """A per-element noise widens the neighbourhood of a boundary; the SwiGLU
+    noise is zero where both inputs sit in their clamped ranges and follows
+    the derivative elsewhere; the W8A8 bound includes the e4m3 contraction's
+    accumulation noise and only ever grows with it."""
+    import oracle.moe as om
+    # 2^-12 relative above a bf16 midpoint: robust without noise, fragile with it
+    mid = 1.0 + 2.0 ** -8
+    h = np.array([[mid * (1 + 2.0 ** -12), 0.3]])
+    assert np.all(om.storage_deviation(h, "bf16")[1] == 0.0)
+    dev = om.storage_deviation(h, "bf16", noise=np.array([[2.0 ** -11, 0.0]]))[1]
+    assert dev[0, 0] == 2.0 ** -7 and dev[0, 1] == 0.0
+    # SwiGLU noise: zero deltas → 0; gate above the limit and up beyond ±limit → 0
+    g = np.array([0.5, -1.0, 9.0, 10.0])
+    u = np.array([0.2, 1.5, 8.0, -9.0])
+    assert np.all(om.swiglu_noise(g, u, 0 * g, 0 * u) == 0.0)
+    n = om.swiglu_noise(g, u, np.full(4, 1e-3), np.full(4, 1e-3))
+    assert n[2] == 0.0 and n[3] == 0.0
+    # away from the clamps it matches |∂h/∂g|·dg + |∂h/∂u|·du to first order
+    a, d = 1.702, 1e-6
+    sig = lambda z: 1.0 / (1.0 + np.exp(-z))
+    for gi, ui in ((0.5, 0.2), (-1.0, 1.5)):
+        dh_dg = (ui + 1.0) * (sig(a * gi) + a * gi * sig(a * gi) * (1 - sig(a * gi)))
+        dh_du = gi * sig(a * gi)
+        lin = abs(dh_dg) * d + abs(dh_du) * d
+        got = om.swiglu_noise(np.array([gi]), np.array([ui]), np.array([d]), np.array([d]))[0]
+        assert got == pytest.approx(lin, rel=1e-4)
+    # the W8A8 bound: larger with the accumulation noise than without it
+    spec, x, lg, w = _w8a8_case()
+    with_noise = ref_moe(x, lg, _w8a8_weights64(w), spec.k, storage="e4m3", act_quant=True, with_bound=True)
+    monkeypatch.setattr(om, "F8_DOT_NOISE", 0.0)
+    without = ref_moe(x, lg, _w8a8_weights64(w), spec.k, storage="e4m3", act_quant=True, with_bound=True)
+    assert np.all(with_noise["out_bound"] >= without["out_bound"])
+    assert np.array_equal(with_noise["out"], without["out"])
+    assert om.F8_DOT_NOISE == 0.0 and 2.0 ** -16 < 2.0 ** -14 < 1e-4
+
+
 def test_finalize_bruteforce_via(fn=ref_moe_finalize):
     """out[t, h] = Σ_j y_slot[t·k + j, h], summed one element at a time in
     mpmath, with slot rows of very different magnitudes."""

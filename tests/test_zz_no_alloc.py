@@ -71,7 +71,7 @@ def test_noalloc_matches_workspace_entry_point(w_dtype, T1, T2):
                   storage="e4m3" if f8 else "bf16", act_quant=f8, with_bound=True)
     rep = compare(host64(got[0]), ref["out"], "e4m3" if f8 else "bf16", slack=ref["out_bound"])
     log(f"    {rep}")
-    assert rep.ok, rep
+    assert rep.ok and rep.normwise <= rep.tol, rep
 
 
 def test_noalloc_graph_replays_match_eager():
