@@ -132,6 +132,15 @@ def test_moe_small(spec):
     run_moe(spec)
 
 
+# the same cases on two more seeds (the 2048-token 256-expert ones aside,
+# for time): the storage-decision bound must hold for other draws too
+@pytest.mark.parametrize("seed", [1, 2])
+@pytest.mark.parametrize("spec", [s for s in SMALL if not s.name.startswith("experts_256_prefill")],
+                         ids=lambda s: s.name)
+def test_moe_small_other_seeds(spec, seed):
+    run_moe(spec, seed=seed)
+
+
 def test_moe_logit_ties_route_to_lower_index():
     spec = MoeSpec("ties", T=96, H=128, I=64, E=16, k=4)
     act = make_moe_activations(spec, 3)
