@@ -38,6 +38,14 @@ token, and the bf16-stored h per slot row) are quantised online with
 s = amax/448 and code = RNE_sat(v / s). Those quantisation decisions are
 taken in fp32 on the stored (bf16) values, the precision the kernel takes
 them in, so both sides pick the same code for the same stored value.
+
+Several results are correct where h lies within the arithmetic noise of a
+storage rounding boundary (the kernel evaluates h in another rounding order,
+and in the W8A8 variant on an fp8 dot product that is not summed as IEEE
+fp32). ``ref_moe(..., with_bound=True)`` returns, per output element, the
+largest change that taking any such decision the other way can cause
+(``storage_deviation``, ``swiglu_noise``, ``F8_DOT_NOISE``); the outputs
+themselves do not depend on it.
 """
 
 import numpy as np
