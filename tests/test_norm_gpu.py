@@ -62,7 +62,8 @@ def test_add_rmsnorm_table_i_batches(T):
 
 
 @pytest.mark.parametrize("T,H,eps,zero_row", [(1, 8, 1e-5, False), (5, 4096, 1e-6, True),
-                                              (3, 136, 0.0, False), (9, 2880, 1e-2, True)])
+                                              (3, 136, 0.0, False), (9, 2880, 1e-2, True),
+                                              (20000, 512, 1e-5, True)])      # a prefill-sized grid
 def test_add_rmsnorm_edge_shapes(T, H, eps, zero_row):
     require_gpu()
     log(f"[add_rmsnorm] T={T} H={H} eps={eps} zero_row={zero_row}")

@@ -81,6 +81,7 @@ def test_rope_table_i_batches(T):
     RopeSpec(5, n_q=3, n_kv=1, D=16, block_size=5, max_pos=97),  # odd sizes, block size 5
     RopeSpec(9, n_q=128, n_kv=16, D=128, block_size=32),        # 1408 items > 1024 threads
     RopeSpec(9, n_q=16, n_kv=4, D=256, block_size=8, interleaved=True),
+    RopeSpec(1024),                                             # a prefill-sized batch of tokens
 ], ids=lambda s: f"T{s.T}_q{s.n_q}_kv{s.n_kv}_D{s.D}_bs{s.block_size}_p{s.max_pos}_il{int(s.interleaved)}")
 def test_rope_geometries(spec):
     run_case(spec, make_rope_inputs(spec, seed=2))
