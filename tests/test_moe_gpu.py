@@ -15,7 +15,8 @@ import numpy as np
 import pytest
 import torch
 
-from oracle import bf16_decode, bf16_encode_rne, compare, e4m3_decode, ref_moe, ref_moe_finalize, ref_quant_rows_e4m3
+from oracle import (bf16_decode, bf16_encode_rne, compare, e4m3_decode, e4m3_encode_rne_sat, ref_moe,
+                    ref_moe_finalize, ref_quant_rows_e4m3)
 from paper_2606_02963_amd import _lib as L
 from paper_2606_02963_amd import api
 from paper_2606_02963_amd.synth import (FINALIZE_BATCHES, FINALIZE_H, FINALIZE_K, MOE_SPECS, MoeSpec,
@@ -245,6 +246,46 @@ def test_quantize_rows_e4m3_long_rows(cols):
     q, s = api.quantize_rows_e4m3(dev_bf16(bits))
     torch.cuda.synchronize()
     q_ref, s_ref = ref_quant_rows_e4m3(bf16_decode(bits))
+    assert np.array_equal(s.cpu().numpy().astype(np.float64), s_ref)
+    assert np.array_equal(q.cpu().numpy(), q_ref)
+
+
+@pytest.mark.parametrize("two_pass", [False, True])
+def test_quantize_rows_e4m3_where_product_and_quotient_differ(two_pass):
+    """Rows holding every bf16 value from amax·2^-16 up to the row maximum
+    amax, for 96 seeded maxima: for about one value per maximum, fp32(v·(1/s))
+    and the correctly rounded fp32(v/s) round to different e4m3 codes (checked
+    here in IEEE float32), so a quantiser that multiplies by the reciprocal
+    must fall back to the quotient there. Positive values only (rows of up to
+    4096 values, one pass from registers) or with their negatives too (rows
+    past 4096 values, two passes)."""
+    require_gpu()
+    rng = np.random.default_rng(11)
+    maxima = bf16_decode(np.sort(rng.choice(np.arange(0x0900, 0x7a00), 96, replace=False)).astype(np.uint16))
+    pos = bf16_decode(np.arange(0x0080, 0x7f80, dtype=np.uint16))
+    rows = []
+    for amax in maxima:
+        v = pos[(pos <= amax) & (pos >= amax * 2.0 ** -16)]
+        rows.append(np.concatenate([[amax], v, -v]) if two_pass else np.concatenate([[amax], v]))
+    cols = -(-max(r.size for r in rows) // 8) * 8
+    assert (cols > 4096) == two_pass
+    x = np.zeros((len(rows), cols))
+    for i, r in enumerate(rows):
+        x[i, :r.size] = r
+    # the rows do hold such values
+    x32 = x.astype(np.float32)
+    sc = (np.abs(x32).max(axis=1, keepdims=True) / np.float32(448.0)).astype(np.float32)
+    quot = (x32 / sc).astype(np.float32)
+    prod = (x32 * (np.float32(1.0) / sc).astype(np.float32)).astype(np.float32)
+    differ = int(np.sum(e4m3_encode_rne_sat(np.clip(quot.astype(np.float64), -448, 448))
+                        != e4m3_encode_rne_sat(np.clip(prod.astype(np.float64), -448, 448))))
+    log(f"[quant] {len(rows)} rows of {cols}: {differ} values where product and quotient round apart")
+    assert differ >= 20
+    bits = to_bf16_bits(x)
+    assert np.array_equal(bf16_decode(bits), x)
+    q, s = api.quantize_rows_e4m3(dev_bf16(bits))
+    torch.cuda.synchronize()
+    q_ref, s_ref = ref_quant_rows_e4m3(x)
     assert np.array_equal(s.cpu().numpy().astype(np.float64), s_ref)
     assert np.array_equal(q.cpu().numpy(), q_ref)
 
