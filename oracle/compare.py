@@ -71,3 +71,22 @@ def compare(y, r, dtype, slack=None):
     max_abs = float(np.max(d)) if d.size else 0.0
     return ComparisonReport(rel_err(y, r, slack), max_abs / mx if mx else max_abs,
                             max_abs, TOL[dtype])
+
+
+def count_above(y, r, dtype, slack=None):
+    """Number of elements whose RMS-floored error, after the optional slack,
+    exceeds the tolerance of ``dtype``."""
+    y = np.asarray(y, dtype=np.float64).ravel()
+    r = np.asarray(r, dtype=np.float64).ravel()
+    if y.shape != r.shape:
+        raise ValueError(f"shape mismatch {y.shape} vs {r.shape}")
+    if r.size == 0:
+        return 0
+    if not np.all(np.isfinite(y)):
+        return int(y.size)
+    rms = float(np.sqrt(np.mean(r * r)))
+    floor = np.maximum(np.abs(r), rms if rms > 0 else 1.0)
+    d = np.abs(y - r)
+    if slack is not None:
+        d = np.maximum(d - np.asarray(slack, dtype=np.float64).ravel(), 0.0)
+    return int(np.sum(d / floor > TOL[dtype]))

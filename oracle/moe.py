@@ -143,16 +143,32 @@ def store_h(h, storage):
 FRAGILE_REL = 2.0 ** -16
 FRAGILE_ABS = 2.0 ** -20
 
-# Accumulation noise of an e4m3 × e4m3 contraction on the matrix cores, as a
-# fraction of Σ|x_i·w_i| over the contraction. The 128-wide fp8 dot product
-# of gfx950's f8f6f4 MFMA is not summed as IEEE fp32: products far below the
-# largest one of the dot product lose low-order bits. Measured: at most
-# 2.4e-5 of Σ|products| on Gaussian data (150 000 dot products), up to
-# 2.6e-4 when one product dominates the other 127. For the W8A8 step the
-# neighbourhood of a storage boundary of h widens by this noise, carried
-# through the clamped SwiGLU; the value is 2.5× the Gaussian-data maximum
-# (the synthetic workloads are Gaussian), not a worst-case bound.
+# Accumulation noise of one 128-wide e4m3 × e4m3 dot product on the matrix
+# cores, as a fraction of its Σ|x_i·w_i|. gfx950's f8f6f4 MFMA does not sum
+# the dot product as IEEE fp32: products far below the largest one lose
+# low-order bits. Measured: at most 2.4e-5 of Σ|products| on Gaussian data
+# (150 000 dot products), up to 2.6e-4 when one product dominates the other
+# 127. A contraction over K runs K/128 such dot products (128 consecutive
+# K-values each) and adds their results in fp32; with sign-mixed data their
+# errors are independent, so the noise of the whole contraction is taken as
+# F8_DOT_NOISE · √(Σ_c S_c²), S_c = Σ|x_i·w_i| over dot product c (see
+# f8_contraction_noise). The value is 2.5× the Gaussian-data maximum (the
+# synthetic workloads are Gaussian), not a worst-case bound.
 F8_DOT_NOISE = 2.0 ** -14
+F8_DOT_K = 128
+
+
+def f8_contraction_noise(X, W):
+    """Noise bound of the e4m3 contraction X·Wᵀ per output element (X [n, K],
+    W [m, K], exact values): F8_DOT_NOISE · √(Σ_c S_c²) over the K/128 dot
+    products of 128 consecutive K-values (a partial last one included)."""
+    aX = np.abs(np.asarray(X, dtype=np.float64))
+    aW = np.abs(np.asarray(W, dtype=np.float64))
+    ss = np.zeros((aX.shape[0], aW.shape[0]))
+    for c0 in range(0, aX.shape[1], F8_DOT_K):
+        s_c = aX[:, c0:c0 + F8_DOT_K] @ aW[:, c0:c0 + F8_DOT_K].T
+        ss += s_c * s_c
+    return F8_DOT_NOISE * np.sqrt(ss)
 
 
 def storage_deviation(h, storage, noise=None):
@@ -192,6 +208,64 @@ def storage_deviation(h, storage, noise=None):
         moved = e4m3_decode(e4m3_encode_rne_sat(f32_round(f32_round(b[r, c]) / sc))) * sc
         dev[r, c] = np.maximum(dev[r, c], np.abs(moved - stored[r, c]))
     return stored, dev
+
+
+def storage_bound(h, storage, W_d, noise=None):
+    """(stored h)·W_dᵀ and, per element of it, the largest change that taking
+    any storage decisions of h within the neighbourhood of a boundary the
+    other way can cause (the neighbourhood as in storage_deviation; each
+    element may take the bf16 value of h − pert, h or h + pert). For e4m3
+    storage the row scale follows the row maximum of whichever values are
+    taken, so its candidates are the scales of every candidate magnitude at
+    or above the smallest maximum any choice gives. Under a candidate scale
+    s′ the rescaling of the whole row, (h(s′) − stored)·W_dᵀ, is taken with
+    its signs and only the element decisions are bounded in absolute value;
+    the largest over the candidates is kept. bf16 storage: deviation·|W_d|ᵀ."""
+    h = np.asarray(h, dtype=np.float64)
+    W_d = np.asarray(W_d, dtype=np.float64)
+    stored, dev = storage_deviation(h, storage, noise)
+    out = stored @ W_d.T
+    if storage != "e4m3":
+        return out, dev @ np.abs(W_d).T
+    pert = FRAGILE_REL * np.abs(h) + FRAGILE_ABS * np.max(np.abs(h), axis=-1, keepdims=True)
+    if noise is not None:
+        pert = pert + np.asarray(noise, dtype=np.float64)
+    bs = (_bf16(h), _bf16(h - pert), _bf16(h + pert))
+    mag = np.stack([np.abs(b) for b in bs])                       # 3 × rows × I
+    floor = mag.min(axis=0).max(axis=-1, keepdims=True)            # smallest maximum any choice gives
+    # an element that may hold the maximum has at most the three values
+    # above: its neighbourhood spans at most two bf16 steps
+    top = mag.max(axis=0) >= floor
+    steps = np.abs(bf16_encode_rne(bs[2]).astype(np.int64) - bf16_encode_rne(bs[1]).astype(np.int64))
+    if np.any(top & ((steps > 2) | (np.sign(bs[1]) * np.sign(bs[2]) < 0))):
+        raise ValueError("storage_bound: a neighbourhood of a row maximum spans more than two bf16 steps")
+    cand = np.where(mag >= floor, mag, -1.0).transpose(1, 0, 2).reshape(h.shape[0], -1)
+    cand = -np.sort(-cand, axis=-1)                                 # candidates first, descending
+    n_c = np.array([np.unique(c[c >= 0]).size for c in cand])
+    width = int(n_c.max())
+    amax = np.empty((h.shape[0], width))
+    for r in range(h.shape[0]):
+        u = np.unique(cand[r][cand[r] >= 0])
+        amax[r] = np.concatenate([u, np.full(width - u.size, u[0])])
+    scales = np.where(amax == 0.0, 1.0, f32_round(amax / E4M3_MAX))
+    # rows with one candidate scale: element decisions only (scale of the stored row)
+    s_ref = ref_quant_rows_e4m3(bs[0])[1]
+    flips = np.zeros_like(h)
+    for b in bs[1:]:
+        flips = np.maximum(flips, np.abs(_dequant_with_scale(b, s_ref) - stored))
+    bound = flips @ np.abs(W_d).T
+    rows = np.flatnonzero(np.any(scales != scales[:, :1], axis=-1) | (scales[:, 0] != s_ref))
+    if rows.size:
+        best = np.zeros((rows.size, W_d.shape[0]))
+        for c in range(width):
+            sc = scales[rows, c]
+            base = _dequant_with_scale(bs[0][rows], sc)
+            fl = np.zeros_like(base)
+            for b in bs[1:]:
+                fl = np.maximum(fl, np.abs(_dequant_with_scale(b[rows], sc) - base))
+            best = np.maximum(best, np.abs((base - stored[rows]) @ W_d.T) + fl @ np.abs(W_d).T)
+        bound[rows] = best
+    return out, bound
 
 
 def swiglu_noise(gate, up, d_gate, d_up, alpha=1.702, limit=7.0):
@@ -249,11 +323,12 @@ def ref_expert_rows(X, W_gu, W_d, storage="bf16", act_quant=False, alpha=1.702,
         noise = None
         if act_quant:
             # the e4m3 contraction's accumulation noise, per element of G
-            dG = F8_DOT_NOISE * (np.abs(X) @ np.abs(np.asarray(W_gu, dtype=np.float64)).T)
+            dG = f8_contraction_noise(X, W_gu)
             d_gate, d_up = _split_gate_up(dG, I, interleaved)
             noise = swiglu_noise(gate, up, d_gate, d_up, alpha, limit)
-        h, dev = storage_deviation(h, storage, noise)
-        return h @ W_d.T, dev @ np.abs(W_d).T
+        out, bound = storage_bound(h, storage, W_d, noise)
+        narrow = bound if noise is None else storage_bound(h, storage, W_d, None)[1]
+        return out, bound, narrow
     return store_h(h, storage) @ W_d.T
 
 
@@ -268,10 +343,13 @@ def ref_moe(x, logits, weights, k, storage="bf16", act_quant=False, alpha=1.702,
     output depends only on its own row and its own routing).
     with_bound: also return "out_bound", per output element the largest
     change any storage-rounding decision of h within the fragile
-    neighbourhood of a boundary (see storage_deviation; with act_quant it
+    neighbourhood of a boundary (see storage_bound; with act_quant it
     includes the e4m3 contraction's accumulation noise, F8_DOT_NOISE) can
     cause; a kernel that evaluates h in another rounding order may take
-    those decisions either way, and every such result is correct.
+    those decisions either way, and every such result is correct. And
+    "out_bound_narrow", the same without the accumulation noise (h within
+    fp32 evaluation noise of the exact value), which only the rare
+    decisions that noise moves may exceed.
     Returns a dict: out [T or len(tokens), H], idx, w, counts, offsets, perm
     (and out_bound).
     """
@@ -289,6 +367,7 @@ def ref_moe(x, logits, weights, k, storage="bf16", act_quant=False, alpha=1.702,
     row_of_token[tok] = np.arange(tok.size)
     y_slot = np.zeros((tok.size * k, H), dtype=np.float64)
     b_slot = np.zeros((tok.size * k, H), dtype=np.float64) if with_bound else None
+    n_slot = np.zeros((tok.size * k, H), dtype=np.float64) if with_bound else None
     for e in range(E):
         slots = perm[offsets[e]:offsets[e + 1]].astype(np.int64)
         slots = slots[row_of_token[slots // k] >= 0]
@@ -297,9 +376,10 @@ def ref_moe(x, logits, weights, k, storage="bf16", act_quant=False, alpha=1.702,
         W_gu, W_d = weights(e)
         dst = row_of_token[slots // k] * k + slots % k
         if with_bound:
-            y, yb = ref_expert_rows(x[slots // k], W_gu, W_d, storage, act_quant, alpha,
-                                    limit, interleaved, with_bound=True)
+            y, yb, yn = ref_expert_rows(x[slots // k], W_gu, W_d, storage, act_quant, alpha,
+                                        limit, interleaved, with_bound=True)
             b_slot[dst] = yb
+            n_slot[dst] = yn
         else:
             y = ref_expert_rows(x[slots // k], W_gu, W_d, storage, act_quant, alpha,
                                 limit, interleaved)
@@ -308,11 +388,14 @@ def ref_moe(x, logits, weights, k, storage="bf16", act_quant=False, alpha=1.702,
     # j ascending, exact until the output
     out = np.zeros((tok.size, H), dtype=np.float64)
     bound = np.zeros((tok.size, H), dtype=np.float64) if with_bound else None
+    narrow = np.zeros((tok.size, H), dtype=np.float64) if with_bound else None
     for j in range(k):
         out += w[tok, j][:, None] * y_slot[j::k]
         if with_bound:
             bound += w[tok, j][:, None] * b_slot[j::k]
+            narrow += w[tok, j][:, None] * n_slot[j::k]
     res = {"out": out, "idx": idx, "w": w, "counts": counts, "offsets": offsets, "perm": perm}
     if with_bound:
         res["out_bound"] = bound
+        res["out_bound_narrow"] = narrow
     return res

@@ -5,6 +5,7 @@ import numpy as np
 import torch
 
 from oracle import bf16_decode
+from oracle.compare import compare, count_above
 
 
 def require_gpu():
@@ -37,3 +38,21 @@ def host64(t):
 
 def log(msg):
     print(msg, flush=True)
+
+
+# share of output elements that may exceed the tolerance after the narrow
+# bound (h within fp32 evaluation noise): the rare storage decisions that the
+# e4m3 MFMA's accumulation noise moves further
+NARROW_EXCESS = 1e-4
+
+
+def check_moe_outputs(got, ref, dtype, label=""):
+    """MoE step outputs against ref_moe(..., with_bound=True): every element
+    within the tolerance after the full legitimate-deviation bound, the
+    normwise error within it without any bound, and at most NARROW_EXCESS of
+    the elements beyond it after the narrow bound."""
+    rep = compare(got, ref["out"], dtype, slack=ref["out_bound"])
+    over = count_above(got, ref["out"], dtype, slack=ref["out_bound_narrow"])
+    log(f"    {label}{rep}; beyond the tolerance after the narrow bound: {over} of {np.size(got)}")
+    assert rep.ok and rep.normwise <= rep.tol and over <= NARROW_EXCESS * np.size(got), f"{label}{rep}, {over} over"
+    return rep

@@ -344,6 +344,18 @@ def test_storage_deviation_noise_and_swiglu_noise(monkeypatch):
         lin = abs(dh_dg) * d + abs(dh_du) * d
         got = om.swiglu_noise(np.array([gi]), np.array([ui]), np.array([d]), np.array([d]))[0]
         assert got == pytest.approx(lin, rel=1e-4)
+    # the contraction noise: one 128-wide dot product gives ε·Σ|x·w|; the dot
+    # products of a longer contraction combine as a root sum of squares, a
+    # partial last one included
+    xs = np.random.default_rng(5).standard_normal((3, 300))
+    ws = np.random.default_rng(6).standard_normal((4, 300))
+    one = om.f8_contraction_noise(xs[:, :128], ws[:, :128])
+    assert np.allclose(one, om.F8_DOT_NOISE * (np.abs(xs[:, :128]) @ np.abs(ws[:, :128]).T), rtol=1e-14)
+    two = om.f8_contraction_noise(np.tile(xs[:, :128], 2), np.tile(ws[:, :128], 2))
+    assert np.allclose(two, np.sqrt(2.0) * one, rtol=1e-14)
+    full = om.f8_contraction_noise(xs, ws)
+    parts = [np.abs(xs[:, a:b]) @ np.abs(ws[:, a:b]).T for a, b in ((0, 128), (128, 256), (256, 300))]
+    assert np.allclose(full, om.F8_DOT_NOISE * np.sqrt(sum(p * p for p in parts)), rtol=1e-14)
     # the W8A8 bound: larger with the accumulation noise than without it
     spec, x, lg, w = _w8a8_case()
     with_noise = ref_moe(x, lg, _w8a8_weights64(w), spec.k, storage="e4m3", act_quant=True, with_bound=True)
@@ -352,6 +364,36 @@ def test_storage_deviation_noise_and_swiglu_noise(monkeypatch):
     assert np.all(with_noise["out_bound"] >= without["out_bound"])
     assert np.array_equal(with_noise["out"], without["out"])
     assert om.F8_DOT_NOISE == 0.0 and 2.0 ** -16 < 2.0 ** -14 < 1e-4
+
+
+def test_storage_bound_covers_sampled_decisions():
+    """Any h′ within the neighbourhood of h (a kernel's h with that error),
+    stored as declared, moves the down projection by no more than
+    storage_bound; the sample includes rows whose e4m3 scale moves and rows
+    whose two largest values are both fragile."""
+    rng = np.random.default_rng(31)
+    h = rng.standard_normal((60, 64)) * 2.0
+    h[::3, 1] = h[::3, 0] = np.max(np.abs(h[::3]), axis=1) * np.array([1.0, -1.0])[rng.integers(0, 2, 20)]
+    W = rng.standard_normal((24, 64)) * 0.05
+    noise = 1e-3 * np.abs(h)
+    pert = om.FRAGILE_REL * np.abs(h) + om.FRAGILE_ABS * np.max(np.abs(h), axis=-1, keepdims=True) + noise
+    for storage in ("bf16", "e4m3"):
+        out, bound = om.storage_bound(h, storage, W, noise)
+        assert np.allclose(out, om.store_h(h, storage) @ W.T, rtol=0, atol=0)
+        moved_scale = 0
+        for trial in range(300):
+            u = rng.uniform(-1.0, 1.0, h.shape) if trial % 2 else rng.choice([-1.0, 1.0], h.shape)
+            h2 = h + u * pert
+            y2 = om.store_h(h2, storage) @ W.T
+            assert np.all(np.abs(y2 - out) <= bound * (1 + 1e-12) + 1e-15), (storage, trial)
+            if storage == "e4m3":
+                moved_scale += int(np.sum(ref_quant_rows_e4m3(bf16_decode(bf16_encode_rne(h2)))[1]
+                                          != ref_quant_rows_e4m3(bf16_decode(bf16_encode_rne(h)))[1]))
+        if storage == "e4m3":
+            assert moved_scale > 100
+    # a neighbourhood wider than two bf16 steps at a row maximum is refused
+    with pytest.raises(ValueError):
+        om.storage_bound(h, "e4m3", W, 0.05 * np.abs(h))
 
 
 def test_finalize_bruteforce_via(fn=ref_moe_finalize):
