@@ -44,8 +44,10 @@ storage rounding boundary (the kernel evaluates h in another rounding order,
 and in the W8A8 variant on an fp8 dot product that is not summed as IEEE
 fp32). ``ref_moe(..., with_bound=True)`` returns, per output element, the
 largest change that taking any such decision the other way can cause
-(``storage_deviation``, ``swiglu_noise``, ``F8_DOT_NOISE``); the outputs
-themselves do not depend on it.
+(``storage_bound``, with the fp8 contraction noise of ``f8_contraction_noise``
+carried through ``swiglu_noise``), and the same for h within fp32 evaluation
+noise only (``out_bound_narrow``); the outputs themselves do not depend on
+either.
 """
 
 import numpy as np
