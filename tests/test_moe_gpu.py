@@ -121,6 +121,13 @@ SMALL = [
     MoeSpec("swiglu_a1_l2_big_e4m3", T=300, H=128, I=128, E=4, k=2, alpha=1.0, limit=2.0, x_std=4.0, w_std=0.05,
             w_dtype="e4m3"),
     MoeSpec("swiglu_limit0", T=64, H=128, I=128, E=4, k=2, limit=0.0),
+    # one expert holding every slot (16 m-tiles, its tiles spread over all
+    # eight XCD ranges of the expert-major order), and every token routed to
+    # both of two experts
+    MoeSpec("one_expert_many_tiles", T=2048, H=256, I=192, E=1, k=1),
+    MoeSpec("one_expert_many_tiles_e4m3", T=2048, H=256, I=192, E=1, k=1, w_dtype="e4m3"),
+    MoeSpec("two_experts_both", T=1000, H=256, I=192, E=2, k=2),
+    MoeSpec("two_experts_both_e4m3", T=1000, H=256, I=192, E=2, k=2, w_dtype="e4m3"),
 ]
 
 
