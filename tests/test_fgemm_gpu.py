@@ -107,6 +107,11 @@ def test_parity_small(spec):
     run_spec(spec)
 
 
+@pytest.mark.parametrize("spec", SMALL, ids=lambda s: s.name)
+def test_parity_small_other_seed(spec):
+    run_spec(spec, seed=1)
+
+
 # Row LogSumExp at small M (the 16 / 64 / 256-row shapes of the one-launch
 # comparison, N = 8192, K = 4096, split-K), ragged rows and columns, one
 # partial n-tile, and a post op.
