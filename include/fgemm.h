@@ -224,7 +224,10 @@ size_t moe_workspace_bytes(const moe_desc *d);
  *   workspace, ws_bytes  at least moe_workspace_bytes(d).
  * Nothing is copied back to the host: the per-expert counts stay on the
  * device and the grouped GEMMs read them there. Arithmetic: fp32
- * accumulation; h (the SwiGLU output) is stored as bf16 (and, with e4m3
+ * accumulation (with e4m3 weights each 128-value dot product of the matrix
+ * cores is summed below fp32 precision: measured within 2.4e-5 of the sum of
+ * its |products| on Gaussian data, up to 2.6e-4 when one product dominates);
+ * h (the SwiGLU output) is stored as bf16 (and, with e4m3
  * weights, quantised per row to e4m3); the per-slot down outputs stay fp32
  * and out is rounded once to bf16 after the weighted sum over j in
  * ascending order, so results are bit-identical from call to call.
