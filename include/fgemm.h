@@ -119,7 +119,10 @@ typedef struct fg_plan fg_plan; /* opaque, host memory, immutable once built */
  *            beyond, since tile operands use 32-bit offsets). FG_E4M3 is the W8A8
  *            form: OCP e4m3fn codes with one fp32 scale per row of x and per
  *            row of W, run with fgemm_run_scaled; the fp8 MFMA accumulates in
- *            fp32 and z = (Σ_k qx·qw)·sx[m]·sw[n] + b before the tail.
+ *            fp32 and z = (Σ_k qx·qw)·sx[m]·sw[n] + b before the tail (each
+ *            128-value dot product is summed below fp32 precision: measured
+ *            within 2.4e-5 of the sum of its |products| on Gaussian data, up
+ *            to 2.6e-4 when one product dominates).
  *   out_dtype FG_F32 or FG_BF16; LogSumExp requires FG_F32. N must be a
  *            multiple of 4 (f32 out) or 8 (bf16 out) (FG_ERR_ALIGNMENT).
  *   epi      the tail (copied into the plan; the caller keeps ownership).
